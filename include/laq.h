@@ -1,0 +1,145 @@
+/*
+ * laq.h -- C ABI of the MI355X (gfx950) W3G128 / W4G128 weight-only quantized
+ * linear library for LAQuant (arXiv 2605.08755).
+ *
+ * LAQuant's deployed model is a standard weight-only quantized model: integer
+ * codes plus a scale and a zero point per group of 128 consecutive weights of
+ * a row, with no online rotation (Sec. 3, "Runtime-Overhead-Free
+ * Quantization"; Sec. 5 efficiency results).  This library provides the two
+ * operations on that model's decode hot path, as hand-written HIP kernels:
+ *
+ *   laq_quantize_w3g128 -- Eq. 1 (Sec. 2): q = clip(round(w/s) + z, 0, 7)
+ *                          with round-to-nearest min-max s, z per 128-group,
+ *                          packed 32 codes per three 32-bit words (App. G).
+ *   laq_linear_w3g128   -- y = x * w_hat^T with w_hat = s * (q - z) (Eq. 1),
+ *                          the fused dequantize GEMV / skinny GEMM of decode
+ *                          (App. G describes the paper's INT3 GEMV).
+ *
+ * plus the W4G128 (4-bit, 8 codes per word) siblings used for bit-width
+ * comparison (Table 3 reports W4G128 and W3G128 decoding).
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ *  - Tensor pointers are DEVICE pointers into memory the caller owns and
+ *    keeps alive until the stream work completes.  The library never
+ *    allocates, frees or synchronizes inside these calls.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Work is enqueued asynchronously; results are valid once the caller
+ *    synchronizes with the stream.
+ *  - Arguments are validated on the host before anything is enqueued.  On
+ *    any error nothing is enqueued and outputs are left untouched; the call
+ *    returns a laq_status and laq_last_error() gives a message.
+ *  - Outputs must not alias inputs.  Weights and activations must be finite.
+ *  - Shapes: N >= 1 output features, K >= 128 input features with
+ *    K % 128 == 0, 1 <= M <= 16 activation rows; N*K < 2^40.
+ *  - Results are deterministic: the same inputs give bitwise-identical
+ *    outputs, call after call.  Calls are thread-safe and may run
+ *    concurrently on different streams.
+ *
+ * Data layout (G = K/128 groups per row, C = K/32 chunks per row)
+ * --------------------------------------------------------------
+ *  w        fp16 [N][K], row-major (PyTorch Linear weight, (out, in)).
+ *  x        fp16 [M][K], row-major.
+ *  y        fp16 [M][N], row-major.
+ *  scales   fp16 [N][G]   -- s of group g of row n at scales[n*G + g].
+ *  zeros    uint8 [N][G]  -- z (0..2^b-1) of group g of row n.
+ *  qweight  W3: uint32 [N][3][C]; W4: uint32 [N][4][C].
+ *    Chunk c of row n covers k = 32c .. 32c+31 and is stored in the words
+ *    P_p = qweight[(n*B + p)*C + c] for planes p = 0..B-1 (B = 3 or 4), so
+ *    32 codes occupy exactly three (W3) or four (W4) 32-bit words.
+ *    W3, code i of the chunk (bits of the code LSB first):
+ *      i < 30: plane i/10; with r = i%10, bits [16*(r%2) + OFF[r/2], +3)
+ *              where OFF = {0, 3, 6, 10, 13};
+ *      i = 30: code bit j is bit 9 of plane j (j = 0, 1, 2);
+ *      i = 31: code bit j is bit 25 of plane j.
+ *    W4, code i of the chunk: plane i/8, bits [16*(i%2) + 4*((i%8)/2), +4).
+ *    Each code pair (2t, 2t+1) thus sits at the same offset in the low and
+ *    high 16-bit halves of a word, inside the fp16 mantissa field, which is
+ *    what lets the GEMV turn one masked word into two fp16 operands.
+ *
+ * Alignment: w, x and qweight 16-byte aligned; scales and y 2-byte aligned.
+ */
+#ifndef LAQ_H
+#define LAQ_H
+
+#include <stdint.h>
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t laq_status;
+
+#define LAQ_OK                0
+#define LAQ_ERR_NULL_POINTER  1  /* a required pointer is NULL               */
+#define LAQ_ERR_BAD_SHAPE     2  /* N < 1, K < 128, K % 128 != 0, too large  */
+#define LAQ_ERR_BAD_M         3  /* M outside 1..16                          */
+#define LAQ_ERR_MISALIGNED    4  /* a pointer violates its alignment         */
+#define LAQ_ERR_HIP           5  /* the HIP runtime reported an error        */
+
+#define LAQ_ABI_VERSION 1
+#define LAQ_GROUP 128
+#define LAQ_MAX_M 16
+
+/* ABI version of the loaded library (LAQ_ABI_VERSION it was built with). */
+int32_t laq_abi_version(void);
+
+/* Static description of a status code. */
+const char *laq_status_string(laq_status status);
+
+/* Detail message of the last failing call on this host thread ("" if none). */
+const char *laq_last_error(void);
+
+/*
+ * laq_quantize_w3g128 -- Eq. 1 (Sec. 2) with round-to-nearest min-max
+ * parameters, per group of 128 consecutive weights of a row.
+ *
+ * For row n and group g, in IEEE fp32 with round-half-to-even:
+ *   lo = min(0, min w), hi = max(0, max w)
+ *   s16 = fp16(fl32(hi - lo) / 7); s16 = 2^-24 if it rounds to zero
+ *   z   = clamp(rint(-lo / s16), 0, 7)
+ *   q   = clamp(rint(w / s16) + z, 0, 7)          (true division)
+ * and writes q packed as described above, s16 to scales and z to zeros.
+ *
+ *   w        [in]  fp16 [N][K]
+ *   qweight  [out] uint32 [N][3][K/32]   (N*K*3/8 bytes)
+ *   scales   [out] fp16 [N][K/128]
+ *   zeros    [out] uint8 [N][K/128]
+ */
+laq_status laq_quantize_w3g128(const void *w, int64_t N, int64_t K,
+                               uint32_t *qweight, void *scales, uint8_t *zeros,
+                               void *stream);
+
+/*
+ * laq_linear_w3g128 -- y[m][n] = sum_k x[m][k] * s[n][g] * (q[n][k] - z[n][g]),
+ * g = k/128: the dequantize-fused GEMV (M = 1) / skinny GEMM (M <= 16) of
+ * decoding.  fp16 inputs, fp32 accumulation, one fp16 round-to-nearest-even
+ * rounding of each output.
+ *
+ *   x        [in]  fp16 [M][K]
+ *   qweight, scales, zeros [in] as written by laq_quantize_w3g128 (or by any
+ *            producer of the same layout, e.g. trained QAT parameters)
+ *   y        [out] fp16 [M][N]
+ */
+laq_status laq_linear_w3g128(const void *x, const uint32_t *qweight,
+                             const void *scales, const uint8_t *zeros,
+                             void *y, int64_t M, int64_t N, int64_t K,
+                             void *stream);
+
+/* W4G128 siblings: same contracts with 4-bit codes (0..15), s = (hi-lo)/15,
+ * qweight uint32 [N][4][K/32] (N*K/2 bytes). */
+laq_status laq_quantize_w4g128(const void *w, int64_t N, int64_t K,
+                               uint32_t *qweight, void *scales, uint8_t *zeros,
+                               void *stream);
+
+laq_status laq_linear_w4g128(const void *x, const uint32_t *qweight,
+                             const void *scales, const uint8_t *zeros,
+                             void *y, int64_t M, int64_t N, int64_t K,
+                             void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAQ_H */
