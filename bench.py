@@ -1,0 +1,274 @@
+"""Decode-step W3G128 linear stack on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+A step is one decode step's worth of quantized linears: the 36-layer
+Qwen3-4B-shaped stack (q, k, v, o, gate, up, down per layer; 252 calls of
+laq_linear_w3g128 at M = 1), captured once into a HIP graph and replayed.
+Weights are synthetic (seeded N(0, 0.02) with 1% x10 outliers, drawn on the
+GPU) and quantized by laq_quantize_w3g128 before timing; activations are
+seeded N(0, 1); everything is resident in HBM before the timed region.
+
+Prints one JSON line.  `value` is the effective weight-stream bandwidth of
+the whole step (packed codes + scales + zeros bytes / step time, graph wall
+time); `roofline` compares the linear kernel's own duration (HIP events at
+kernel start/end) with the 8 TB/s HBM peak; `cpu_baseline` times the CPU
+oracle on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "µs/decode-step linear stack + effective weight GB/s (% of HBM peak), M=1"
+HBM_PEAK_GBS = 8000.0
+GROUP = 128
+
+
+def bytes_per_weight(bits):
+    # codes + fp16 scale + uint8 zero per 128-group
+    return bits / 8 + 2 / GROUP + 1 / GROUP
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+class Stack:
+    """All quantized projections of a workload, resident on the GPU."""
+
+    def __init__(self, workload, device, bits_list=(3,), keep_fp16=False):
+        import torch
+        from paper_2605_08755_amd import inputs, laq
+        spec = inputs.WORKLOADS[workload]
+        self.workload = workload
+        self.layers = spec["layers"]
+        self.projs = spec["projs"]
+        self.device = device
+        self.q = {b: [] for b in bits_list}
+        self.fp16 = [] if keep_fp16 else None
+        self.shapes = []
+        for layer in range(self.layers):
+            for pi, (name, N, K) in enumerate(self.projs):
+                w = inputs.weights_torch(N, K, seed=layer * 16 + pi, device=device)
+                for b in bits_list:
+                    self.q[b].append(laq.quantize(w, b))
+                if keep_fp16:
+                    self.fp16.append(w)
+                del w
+                self.shapes.append((layer, name, N, K))
+        torch.cuda.synchronize()
+        self.x = {}
+        slots = sorted({(layer, inputs.X_SLOT.get(name, 0), K) for (layer, name, N, K) in self.shapes})
+        for (layer, slot, K) in slots:
+            self.x[(layer, slot)] = inputs.activations_torch(16, K, seed=layer * 8 + slot, device=device)
+        self.y = [torch.empty((16, N), dtype=torch.float16, device=device) for (_, _, N, _) in self.shapes]
+        self.slot_of = [inputs.X_SLOT.get(name, 0) for (_, name, _, _) in self.shapes]
+
+    def weights(self):
+        return sum(N * K for (_, _, N, K) in self.shapes)
+
+    def weight_bytes(self, bits):
+        return self.weights() * bytes_per_weight(bits)
+
+    def step(self, M, bits, events=None):
+        from paper_2605_08755_amd import laq
+        for i, (layer, name, N, K) in enumerate(self.shapes):
+            q, s, z = self.q[bits][i]
+            if events is not None:
+                laq.profile_next_launch(*events[i])
+            laq.linear(self.x[(layer, self.slot_of[i])][:M], q, s, z, bits, out=self.y[i][:M])
+
+
+def time_graph(stack, M, bits, steps, warmup):
+    """Capture one step into a HIP graph; time `steps` replays."""
+    import torch
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    stack.step(M, bits)  # eager warm-up (loads code objects)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        stack.step(M, bits)
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / steps
+    del g
+    return ms, wall
+
+
+def kernel_durations(stack, M, bits, reps):
+    """Per-launch kernel durations (ms) from events recorded at kernel start/end."""
+    import torch
+    n = len(stack.shapes)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in ev:  # materialize the underlying hipEvents
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    tot = [0.0] * n
+    for _ in range(reps):
+        stack.step(M, bits, events=ev)
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(ev):
+            tot[i] += a.elapsed_time(b)
+    return [t / reps for t in tot]
+
+
+def cpu_baseline(budget_s=12.0):
+    """The CPU oracle (as it stands) on a bounded sample: layer 0 of the
+    Qwen3-4B stack (7 projections, M = 1), repeated for ~budget_s seconds."""
+    import numpy as np
+    import oracle
+    from paper_2605_08755_amd import inputs
+    cases = []
+    for pi, (name, N, K) in enumerate(inputs.QWEN3_4B):
+        w = inputs.weights(N, K, cfg=3, layer=0, proj=pi)
+        codes, s, z = oracle.quantize(w, 3)
+        x = inputs.activations(1, K, cfg=3, layer=0, slot=inputs.X_SLOT[name])
+        cases.append((x, codes, s, z, N * K))
+        del w
+    weights = sum(c[4] for c in cases)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        for (x, codes, s, z, _) in cases:
+            oracle.linear(x, codes, s, z)
+        reps += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = (time.perf_counter() - t0) / reps
+    gbs = weights * bytes_per_weight(3) / dt / 1e9
+    return {"value": round(gbs, 3), "unit": "GB/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "layer 0 of the 36-layer Qwen3-4B-shaped stack: 7 W3G128 projections "
+                      "(%d weights) at M=1, oracle fp64 linear on its own codes, %d repetitions "
+                      "in %.1f s; %.1f ms per layer, i.e. %.0f ms per 36-layer step"
+                      % (weights, reps, dt * reps, dt * 1e3, dt * 36e3),
+            "us_per_step_equiv": round(dt * 36e6, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="stack4b")
+    ap.add_argument("--profile-reps", type=int, default=5)
+    ap.add_argument("--no-sweep", action="store_true", help="skip the M x bits sweep and quantize timing")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this library's path runs on a single MI355X "
+              "(multi-GPU sharding is a design note, not built); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_08755_amd import laq
+    laq.lib()  # fails loudly when liblaq.so is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    bits_list = (3,) if args.no_sweep else (3, 4)
+    log("building %s (bits %s) ..." % (args.workload, bits_list))
+    t0 = time.perf_counter()
+    stack = Stack(args.workload, dev, bits_list=bits_list, keep_fp16=not args.no_sweep)
+    log("built in %.1f s: %d linears, %.3f G weights" % (time.perf_counter() - t0, len(stack.shapes), stack.weights() / 1e9))
+
+    # ---- headline: W3, M = 1, graph replay
+    wbytes = stack.weight_bytes(3)
+    ms, wall = time_graph(stack, 1, 3, args.steps, args.warmup)
+    value = wbytes / (ms * 1e-3) / 1e9
+    log("W3 M=1: %.1f us/step, %.1f GB/s (%.1f%% of 8 TB/s)" % (ms * 1e3, value, value / HBM_PEAK_GBS * 100))
+
+    # ---- kernel-level: the linear kernel's own durations
+    durs = kernel_durations(stack, 1, 3, args.profile_reps)
+    ksum_ms = sum(durs)
+    achieved = wbytes / (ksum_ms * 1e-3) / 1e9
+    per_proj = {}
+    for (layer, name, N, K), d in zip(stack.shapes, durs):
+        p = per_proj.setdefault(name, {"N": N, "K": K, "us": 0.0, "n": 0})
+        p["us"] += d * 1e3
+        p["n"] += 1
+    for name, p in per_proj.items():
+        p["us"] = round(p["us"] / p["n"], 3)
+        p["GBps"] = round(p["N"] * p["K"] * bytes_per_weight(3) / (p["us"] * 1e-6) / 1e9, 1)
+        del p["n"]
+    log("kernel sum %.1f us/step -> %.1f GB/s; per proj %s" % (ksum_ms * 1e3, achieved, per_proj))
+
+    extra = {"us_per_step_graph": round(ms * 1e3, 2), "pct_of_hbm_peak": round(value / HBM_PEAK_GBS * 100, 2),
+             "kernel_sum_us_per_step": round(ksum_ms * 1e3, 2), "launches_per_step": len(stack.shapes),
+             "avg_kernel_us": round(ksum_ms * 1e3 / len(stack.shapes), 3), "per_projection": per_proj,
+             "wall_s_timed_region": round(wall, 4)}
+
+    if not args.no_sweep:
+        sweep = {}
+        for bits in (3, 4):
+            for M in (1, 4, 8, 16):
+                ms_b, _ = time_graph(stack, M, bits, max(20, args.steps // 4), 5)
+                sweep["w%d_m%d" % (bits, M)] = {"us": round(ms_b * 1e3, 2),
+                                                "GBps": round(stack.weight_bytes(bits) / (ms_b * 1e-3) / 1e9, 1)}
+        extra["sweep"] = sweep
+        log("sweep", sweep)
+        # quantize throughput over the whole stack (fp16 read + packed write)
+        qd = []
+        for bits in (3, 4):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            outs = stack.q[bits]
+            for i, w in enumerate(stack.fp16):  # warm
+                laq.quantize(w, bits, out=outs[i])
+            torch.cuda.synchronize()
+            e0.record()
+            for i, w in enumerate(stack.fp16):
+                laq.quantize(w, bits, out=outs[i])
+            e1.record()
+            torch.cuda.synchronize()
+            qms = e0.elapsed_time(e1)
+            qbytes = stack.weights() * (2 + bytes_per_weight(bits))
+            qd.append(("w%d" % bits, {"ms": round(qms, 3), "GBps": round(qbytes / (qms * 1e-3) / 1e9, 1)}))
+        extra["quantize_stack"] = dict(qd)
+        log("quantize", extra["quantize_stack"])
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "stack4b: 36-layer Qwen3-4B-shaped decode-step linear stack "
+                               "(q,k,v,o,gate,up,down per layer), W3G128, M=1",
+                   "layers": stack.layers, "linears_per_step": len(stack.shapes), "M": 1, "bits": 3,
+                   "group": GROUP, "weights_per_step": stack.weights(),
+                   "weight_bytes_per_step": int(round(wbytes))},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "linear_kernel<3,1> (W3G128 GEMV, M=1)"},
+        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(),
+        "extra": extra,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

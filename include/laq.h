@@ -92,6 +92,17 @@ const char *laq_status_string(laq_status status);
 const char *laq_last_error(void);
 
 /*
+ * laq_profile_next_launch -- measurement hook, not needed for normal use.
+ * The next laq_quantize_* / laq_linear_* call made on this host thread
+ * records `start_event` when its kernel starts executing and `stop_event`
+ * when it ends (hipEvent_t handles created by the caller, passed as void*;
+ * either may be NULL), so hipEventElapsedTime gives the kernel's own
+ * duration without launch gaps.  The hook is then cleared.  A call that
+ * fails validation also clears it.  Always returns LAQ_OK.
+ */
+laq_status laq_profile_next_launch(void *start_event, void *stop_event);
+
+/*
  * laq_quantize_w3g128 -- Eq. 1 (Sec. 2) with round-to-nearest min-max
  * parameters, per group of 128 consecutive weights of a row.
  *

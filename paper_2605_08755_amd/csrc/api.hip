@@ -1,0 +1,128 @@
+// C ABI of the library (include/laq.h): argument validation on the host,
+// then an asynchronous launch on the caller's stream.  Nothing is enqueued
+// when validation fails.
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "laq.h"
+#include "laq_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local laq::LaunchEvents g_next_events;  // measurement hook, consumed by the next launch
+
+laq::LaunchEvents take_events() {
+  laq::LaunchEvents ev = g_next_events;
+  g_next_events = laq::LaunchEvents{};
+  return ev;
+}
+
+laq_status fail(laq_status st, const char* fn, const char* what) {
+  char buf[256];
+  std::snprintf(buf, sizeof(buf), "%s: %s", fn, what);
+  g_last_error = buf;
+  return st;
+}
+
+laq_status ok() {
+  g_last_error.clear();
+  return LAQ_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+laq_status check_shape(const char* fn, int64_t N, int64_t K) {
+  if (N < 1) return fail(LAQ_ERR_BAD_SHAPE, fn, "N must be >= 1");
+  if (K < 128 || K % 128 != 0) return fail(LAQ_ERR_BAD_SHAPE, fn, "K must be a positive multiple of 128");
+  if (N > 0x7FFFFFFFLL) return fail(LAQ_ERR_BAD_SHAPE, fn, "N must be < 2^31");
+  if (K > (1LL << 24)) return fail(LAQ_ERR_BAD_SHAPE, fn, "K must be <= 2^24");
+  if (N * K >= (1LL << 40)) return fail(LAQ_ERR_BAD_SHAPE, fn, "N*K must be < 2^40");
+  return LAQ_OK;
+}
+
+laq_status hip_status(const char* fn, hipError_t e) {
+  if (e != hipSuccess) return fail(LAQ_ERR_HIP, fn, hipGetErrorString(e));
+  return ok();
+}
+
+template <int BITS>
+laq_status quantize(const char* fn, const void* w, int64_t N, int64_t K, uint32_t* qweight,
+                    void* scales, uint8_t* zeros, void* stream) {
+  const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
+  if (!w || !qweight || !scales || !zeros) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (!aligned(w, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "w and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales must be 2-byte aligned");
+  return hip_status(fn, laq::launch_quantize<BITS>(static_cast<const uint16_t*>(w), N, K, qweight,
+                                                   static_cast<uint16_t*>(scales), zeros,
+                                                   static_cast<hipStream_t>(stream), ev));
+}
+
+template <int BITS>
+laq_status linear(const char* fn, const void* x, const uint32_t* qweight, const void* scales,
+                  const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {
+  const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
+  if (!x || !qweight || !scales || !zeros || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (M < 1 || M > LAQ_MAX_M) return fail(LAQ_ERR_BAD_M, fn, "M must be in 1..16");
+  if (!aligned(x, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "x and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  return hip_status(fn, laq::launch_linear<BITS>(static_cast<const uint16_t*>(x), qweight,
+                                                 static_cast<const uint16_t*>(scales), zeros,
+                                                 static_cast<uint16_t*>(y), (int)M, N, K,
+                                                 static_cast<hipStream_t>(stream), ev));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t laq_abi_version(void) { return LAQ_ABI_VERSION; }
+
+const char* laq_status_string(laq_status status) {
+  switch (status) {
+    case LAQ_OK: return "ok";
+    case LAQ_ERR_NULL_POINTER: return "null pointer argument";
+    case LAQ_ERR_BAD_SHAPE: return "bad shape (need N >= 1, K >= 128, K % 128 == 0)";
+    case LAQ_ERR_BAD_M: return "M outside 1..16";
+    case LAQ_ERR_MISALIGNED: return "misaligned pointer";
+    case LAQ_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* laq_last_error(void) { return g_last_error.c_str(); }
+
+laq_status laq_profile_next_launch(void* start_event, void* stop_event) {
+  g_next_events.start = static_cast<hipEvent_t>(start_event);
+  g_next_events.stop = static_cast<hipEvent_t>(stop_event);
+  return LAQ_OK;
+}
+
+laq_status laq_quantize_w3g128(const void* w, int64_t N, int64_t K, uint32_t* qweight, void* scales,
+                               uint8_t* zeros, void* stream) {
+  return quantize<3>("laq_quantize_w3g128", w, N, K, qweight, scales, zeros, stream);
+}
+
+laq_status laq_quantize_w4g128(const void* w, int64_t N, int64_t K, uint32_t* qweight, void* scales,
+                               uint8_t* zeros, void* stream) {
+  return quantize<4>("laq_quantize_w4g128", w, N, K, qweight, scales, zeros, stream);
+}
+
+laq_status laq_linear_w3g128(const void* x, const uint32_t* qweight, const void* scales,
+                             const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                             void* stream) {
+  return linear<3>("laq_linear_w3g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+laq_status laq_linear_w4g128(const void* x, const uint32_t* qweight, const void* scales,
+                             const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                             void* stream) {
+  return linear<4>("laq_linear_w4g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,46 @@
+// Internal declarations shared by the library's translation units (not part
+// of the public ABI; the public contract is include/laq.h).
+#pragma once
+
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace laq {
+
+// Native 128-bit vector (usable with the nontemporal load builtins).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// fp16 pair as the operand type of v_dot2_f32_f16.
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ half2_t as_half2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
+
+// Optional events recorded at the kernel's execution start and end
+// (hipExtLaunchKernelGGL); both null for an ordinary launch.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t stream,
+                   const LaunchEvents& ev, Args... args) {
+  if (ev.start || ev.stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, stream, ev.start, ev.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
+}
+
+// Launchers (return the HIP error of the launch; shapes already validated).
+template <int BITS>
+hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qweight,
+                           uint16_t* scales, uint8_t* zeros, hipStream_t stream,
+                           const LaunchEvents& ev);
+
+template <int BITS>
+hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
+                         const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
+                         hipStream_t stream, const LaunchEvents& ev);
+
+}  // namespace laq

@@ -1,0 +1,140 @@
+"""Python binding of liblaq.so (the C ABI in include/laq.h).
+
+Argument marshalling only: every step of quantize and linear runs in the HIP
+kernels of liblaq.so.  torch provides device memory and the current stream.
+There is no fallback: if the library is missing or a call fails, an
+exception is raised.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblaq.so")
+
+LAQ_OK = 0
+LAQ_ERR_NULL_POINTER = 1
+LAQ_ERR_BAD_SHAPE = 2
+LAQ_ERR_BAD_M = 3
+LAQ_ERR_MISALIGNED = 4
+LAQ_ERR_HIP = 5
+MAX_M = 16
+GROUP = 128
+
+EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profile_next_launch",
+           "laq_quantize_w3g128", "laq_linear_w3g128",
+           "laq_quantize_w4g128", "laq_linear_w4g128")
+
+_lib = None
+
+
+class LaqError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__("laq status %d: %s" % (status, message))
+        self.status = status
+
+
+def lib():
+    """Load liblaq.so (built by paper_2605_08755_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("liblaq.so not built: run `python -m paper_2605_08755_amd.build` "
+                              "(there is no non-HIP fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I64 = ctypes.c_void_p, ctypes.c_int64
+        L.laq_abi_version.argtypes = []
+        L.laq_abi_version.restype = ctypes.c_int32
+        L.laq_status_string.argtypes = [ctypes.c_int32]
+        L.laq_status_string.restype = ctypes.c_char_p
+        L.laq_last_error.argtypes = []
+        L.laq_last_error.restype = ctypes.c_char_p
+        L.laq_profile_next_launch.argtypes = [P, P]
+        L.laq_profile_next_launch.restype = ctypes.c_int32
+        for name in ("laq_quantize_w3g128", "laq_quantize_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [P, I64, I64, P, P, P, P]
+            f.restype = ctypes.c_int32
+        for name in ("laq_linear_w3g128", "laq_linear_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [P, P, P, P, P, I64, I64, I64, P]
+            f.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != LAQ_OK:
+        raise LaqError(status, lib().laq_last_error().decode())
+
+
+def _stream(device):
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def profile_next_launch(start_event, stop_event):
+    """Have the next quantize/linear call on this thread record the given
+    torch.cuda.Event pair at its kernel's execution start and end."""
+    _check(lib().laq_profile_next_launch(ctypes.c_void_p(start_event.cuda_event),
+                                         ctypes.c_void_p(stop_event.cuda_event)))
+
+
+def packed_words(bits, N, K):
+    """Number of uint32 words of a packed [N][K] matrix."""
+    return N * bits * (K // 32)
+
+
+def quantize(w, bits=3, out=None):
+    """Quantize fp16 [N][K] weights on the GPU (Eq. 1, RTN min-max per 128-group).
+
+    Returns (qweight int32 [N][bits][K/32], scales fp16 [N][K/128],
+    zeros uint8 [N][K/128]).  qweight holds uint32 bit patterns in an int32
+    tensor (torch has no uint32 arithmetic).
+    """
+    import torch
+    assert w.is_cuda and w.dtype == torch.float16 and w.dim() == 2 and w.is_contiguous()
+    N, K = w.shape
+    if out is None:
+        qweight = torch.empty((N, bits, K // 32), dtype=torch.int32, device=w.device)
+        scales = torch.empty((N, K // GROUP), dtype=torch.float16, device=w.device)
+        zeros = torch.empty((N, K // GROUP), dtype=torch.uint8, device=w.device)
+    else:
+        qweight, scales, zeros = out
+    fn = lib().laq_quantize_w3g128 if bits == 3 else lib().laq_quantize_w4g128
+    _check(fn(_ptr(w), N, K, _ptr(qweight), _ptr(scales), _ptr(zeros), _stream(w.device)))
+    return qweight, scales, zeros
+
+
+def linear(x, qweight, scales, zeros, bits=3, out=None):
+    """y = x @ w_hat^T for fp16 x [M][K] (M <= 16) against packed weights."""
+    import torch
+    assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+    M, K = x.shape
+    N = scales.shape[0]
+    assert qweight.numel() == packed_words(bits, N, K) and qweight.is_contiguous()
+    assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+    assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+    y = torch.empty((M, N), dtype=torch.float16, device=x.device) if out is None else out
+    fn = lib().laq_linear_w3g128 if bits == 3 else lib().laq_linear_w4g128
+    _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _stream(x.device)))
+    return y
+
+
+def quantize_w3g128(w, out=None):
+    return quantize(w, 3, out)
+
+
+def linear_w3g128(x, qweight, scales, zeros, out=None):
+    return linear(x, qweight, scales, zeros, 3, out)
+
+
+def quantize_w4g128(w, out=None):
+    return quantize(w, 4, out)
+
+
+def linear_w4g128(x, qweight, scales, zeros, out=None):
+    return linear(x, qweight, scales, zeros, 4, out)

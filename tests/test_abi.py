@@ -1,0 +1,100 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol
+include/laq.h declares, and rejects bad arguments on the host (before any
+HIP call, so nothing is launched).  Pointers used here are never
+dereferenced: each call fails validation first."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_08755_amd import laq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "laq.h")
+
+FAKE = 0x100000  # 16-byte aligned, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(laq_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return laq.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) >= 7
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(laq.EXPORTS) == set(names)
+
+
+def test_version_and_strings(L):
+    assert L.laq_abi_version() == 1
+    for s in range(0, 6):
+        assert L.laq_status_string(s)
+    assert L.laq_status_string(99) == b"unknown status"
+
+
+def _quant(L, bits, w=FAKE, N=4, K=128, q=FAKE, s=FAKE, z=FAKE):
+    f = L.laq_quantize_w3g128 if bits == 3 else L.laq_quantize_w4g128
+    return f(ctypes.c_void_p(w), N, K, ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z), None)
+
+
+def _lin(L, bits, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, M=1, N=4, K=128):
+    f = L.laq_linear_w3g128 if bits == 3 else L.laq_linear_w4g128
+    return f(ctypes.c_void_p(x), ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z),
+             ctypes.c_void_p(y), M, N, K, None)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_quantize_validation(L, bits):
+    assert _quant(L, bits, w=0) == laq.LAQ_ERR_NULL_POINTER
+    assert _quant(L, bits, q=0) == laq.LAQ_ERR_NULL_POINTER
+    assert _quant(L, bits, s=0) == laq.LAQ_ERR_NULL_POINTER
+    assert _quant(L, bits, z=0) == laq.LAQ_ERR_NULL_POINTER
+    assert _quant(L, bits, N=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, N=-3) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, K=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, K=64) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, K=200) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, N=1 << 31) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, N=1 << 30, K=1 << 11) == laq.LAQ_ERR_BAD_SHAPE
+    assert _quant(L, bits, w=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert _quant(L, bits, q=FAKE + 4) == laq.LAQ_ERR_MISALIGNED
+    assert _quant(L, bits, s=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_quantize" in L.laq_last_error()
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_validation(L, bits):
+    for kw in ("x", "q", "s", "z", "y"):
+        assert _lin(L, bits, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _lin(L, bits, M=0) == laq.LAQ_ERR_BAD_M
+    assert _lin(L, bits, M=17) == laq.LAQ_ERR_BAD_M
+    assert _lin(L, bits, M=-1) == laq.LAQ_ERR_BAD_M
+    assert _lin(L, bits, N=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lin(L, bits, K=127) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lin(L, bits, K=384 + 32) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lin(L, bits, x=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert _lin(L, bits, q=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert _lin(L, bits, s=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert _lin(L, bits, y=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_linear" in L.laq_last_error()
+
+
+def test_shape_check_precedes_m_check(L):
+    # a bad shape is reported even when M is also bad
+    assert _lin(L, 3, M=0, K=100) == laq.LAQ_ERR_BAD_SHAPE
+
+
+def test_packed_sizes():
+    # 32 three-bit codes in three words: N*K*3/32 words; W4: N*K/8 words
+    assert laq.packed_words(3, 1024, 1024) * 4 == 1024 * 1024 * 3 // 8
+    assert laq.packed_words(4, 1024, 1024) * 4 == 1024 * 1024 // 2

@@ -1,0 +1,272 @@
+"""GPU parity: the HIP kernels (through the C ABI) against the CPU oracle.
+
+Quantize: packed words, scale bits and zero bytes bit-exact.
+Linear:   each fp16 output is an fp16 rounding of a value within
+          1e-3 x RMS of the oracle's exact fp64 result (oracle/compare.py).
+Inputs are seeded (paper_2605_08755_amd.inputs); the linear is fed the
+oracle's own quantization, so its parity does not depend on the quantize
+kernel.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.compare import linear_check
+from paper_2605_08755_amd import inputs, laq
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print("[gpu-case]", *a, flush=True)
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def gpu_quantize(w16, bits):
+    q, s, z = laq.quantize(to_dev(w16), bits)
+    torch.cuda.synchronize()
+    return (q.cpu().numpy().view(np.uint32), s.cpu().numpy().view(np.uint16), z.cpu().numpy())
+
+
+def oracle_packed(w16, bits):
+    codes, s, z = oracle.quantize(w16, bits)
+    return codes, oracle.pack(codes, bits), s, z
+
+
+def gpu_linear(x16, qw, s, z, bits):
+    y = laq.linear(to_dev(x16), to_dev(qw.view(np.int32)), to_dev(s.view(np.float16)), to_dev(z), bits)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+# ---------------------------------------------------------------------------
+# quantize
+# ---------------------------------------------------------------------------
+QSHAPES = [(1, 128), (17, 384), (33, 2560), (5, 9728), (1024, 1024), (300, 4096), (2, 25600)]
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("N,K", QSHAPES)
+def test_quantize_bitexact(bits, N, K):
+    say("quantize", bits, N, K)
+    w = inputs.weights(N, K, cfg=10, layer=N, proj=K % 97)
+    codes, qw, s, z = oracle_packed(w, bits)
+    gq, gs, gz = gpu_quantize(w, bits)
+    assert np.array_equal(gs, s), "scales differ"
+    assert np.array_equal(gz, z), "zeros differ"
+    assert np.array_equal(gq, qw), "packed codes differ"
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_quantize_special_groups(bits):
+    say("quantize special", bits)
+    qmax = (1 << bits) - 1
+    K = 384
+    rows = []
+    rows.append(np.zeros(K))                                   # all zero
+    rows.append(np.full(K, 0.75))                              # constant positive
+    rows.append(-np.linspace(0.01, 0.5, K))                    # all negative
+    r = np.zeros(K); r[17] = -3.0; rows.append(r)              # single outlier
+    r = np.zeros(K); r[:5] = [6e-8, -6e-8, 1.2e-7, 0, -1.8e-7]; rows.append(r)  # subnormal range
+    r = np.zeros(K); r[0], r[1] = -3 / 64, 4 / 64
+    r[2:12] = np.array([2.5, 1.5, -0.5, 0.5, 3.5, -2.5, -1.5, 4.0, -3.0, 0.0]) / 64
+    rows.append(r)                                             # exact ties (W3 grid)
+    rng = np.random.default_rng(3)
+    for e in (-14, -3, 5):                                     # on-grid groups
+        z0 = int(rng.integers(0, qmax + 1))
+        j = rng.integers(0, qmax + 1, K); j[0], j[1] = 0, qmax
+        rows.append(np.ldexp((j - z0).astype(np.float64), e))
+    rows.append(np.full(K, 65504.0))                           # largest half
+    r = np.full(K, -65504.0); r[::2] = 65504.0; rows.append(r)  # widest range
+    rows.append(np.full(K, -0.0))                              # negative zeros
+    w = np.array(rows).astype(np.float16)
+    codes, qw, s, z = oracle_packed(w, bits)
+    gq, gs, gz = gpu_quantize(w, bits)
+    assert np.array_equal(gs, s) and np.array_equal(gz, z) and np.array_equal(gq, qw)
+
+
+def test_quantize_canary():
+    """Writes stay inside the outputs: sentinels around them are untouched."""
+    say("quantize canary")
+    N, K = 37, 640
+    w = to_dev(inputs.weights(N, K, cfg=11))
+    words = laq.packed_words(3, N, K)
+    G = K // 128
+    qbuf = torch.full((words + 64,), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+    sbuf = torch.full((N * G + 64,), 7.0, dtype=torch.float16, device=DEV)
+    zbuf = torch.full((N * G + 64,), 0xEE, dtype=torch.uint8, device=DEV)
+    laq.quantize(w, 3, out=(qbuf[:words], sbuf[:N * G].view(N, G), zbuf[:N * G].view(N, G)))
+    torch.cuda.synchronize()
+    assert torch.all(qbuf[words:] == 0x5A5A5A5A)
+    assert torch.all(sbuf[N * G:] == 7.0)
+    assert torch.all(zbuf[N * G:] == 0xEE)
+
+
+# ---------------------------------------------------------------------------
+# linear
+# ---------------------------------------------------------------------------
+LSHAPES = [(1, 128), (17, 384), (64, 128), (300, 2560), (1024, 1024), (257, 4096), (96, 9728)]
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 8, 11, 16])
+@pytest.mark.parametrize("N,K", LSHAPES)
+def test_linear_parity(bits, M, N, K):
+    say("linear", bits, M, N, K)
+    w = inputs.weights(N, K, cfg=12, layer=M, proj=N % 89)
+    x = inputs.activations(M, K, cfg=12, layer=N)
+    codes, qw, s, z = oracle_packed(w, bits)
+    y = gpu_linear(x, qw, s, z, bits)
+    ref = oracle.linear(x, codes, s, z)
+    r = linear_check(y, ref)
+    assert r["ok"], r
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_onehot_bitwise(bits):
+    """x = e_k picks one exact term: y == fp16(w_hat[:, k]) bitwise."""
+    say("linear onehot", bits)
+    N, K = 200, 1280
+    w = inputs.weights(N, K, cfg=13)
+    codes, qw, s, z = oracle_packed(w, bits)
+    wh = oracle.dequant(codes, s, z)
+    for k in (0, 1, 29, 30, 31, 32, 127, 128, 555, K - 2, K - 1):
+        x = np.zeros((1, K), np.float16)
+        x[0, k] = 1.0
+        y = gpu_linear(x, qw, s, z, bits)
+        assert np.array_equal(y[0], wh[:, k].astype(np.float16)), k
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_zero_codes_and_scaling(bits):
+    say("linear zero/pow2", bits)
+    M, N, K = 4, 130, 768
+    w = inputs.weights(N, K, cfg=14)
+    x = inputs.activations(M, K, cfg=14)
+    codes, qw, s, z = oracle_packed(w, bits)
+    # all-zero weights quantize to codes 0, zero point 0: y is exactly zero
+    wz = np.zeros((N, K), np.float16)
+    cz, qz, sz, zz = oracle_packed(wz, bits)
+    assert np.all(gpu_linear(x, qz, sz, zz, bits) == 0)
+    # codes equal to a nonzero zero point (a state quantize never produces):
+    # the kernel forms sum x*q and z*sum x separately, so the result is the
+    # fp32 rounding residue of that cancellation, bounded by a few fp32 ulps
+    # of s*z*sum|x| per group (v_dot2_f32_f16 does not round each step to
+    # nearest; see the design notes)
+    c0 = np.repeat(z, 128, axis=1).astype(np.uint8)
+    y0 = gpu_linear(x, oracle.pack(c0, bits), s, z, bits).astype(np.float64)
+    sv = oracle.f16_to_f32(s).astype(np.float64)
+    ax = np.abs(x.astype(np.float64)).reshape(M, K // 128, 128).sum(axis=2)      # [M][G]
+    bound = (ax[:, None, :] * (sv * z)[None, :, :]).sum(axis=2) * 2.0 ** -16      # [M][N]
+    assert np.all(np.abs(y0) <= bound + 2.0 ** -24), float(np.max(np.abs(y0) / (bound + 1e-30)))
+    # y(4x) == 4 y(x) bitwise (power-of-two scaling is exact end to end)
+    y1 = gpu_linear(x, qw, s, z, bits)
+    y4 = gpu_linear((x.astype(np.float32) * 4).astype(np.float16), qw, s, z, bits)
+    assert np.array_equal(y4, (y1.astype(np.float32) * 4).astype(np.float16))
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_rows_consistent_and_deterministic(bits):
+    say("linear rows/determinism", bits)
+    N, K = 512, 2560
+    w = inputs.weights(N, K, cfg=15)
+    x = inputs.activations(16, K, cfg=15)
+    codes, qw, s, z = oracle_packed(w, bits)
+    y16 = gpu_linear(x, qw, s, z, bits)
+    y16b = gpu_linear(x, qw, s, z, bits)
+    assert np.array_equal(y16, y16b)
+    ref = oracle.linear(x, codes, s, z)
+    for m in (0, 7, 15):
+        y1 = gpu_linear(x[m:m + 1], qw, s, z, bits)
+        assert linear_check(y1[0], ref[m])["ok"]
+        # both are within tolerance of the same exact value
+        assert np.max(np.abs(y1[0].astype(np.float64) - y16[m])) <= 2e-3 * np.sqrt(np.mean(ref[m] ** 2)) + \
+            np.max(np.abs(ref[m])) * 2 ** -10
+
+
+def test_linear_canary():
+    say("linear canary")
+    M, N, K = 3, 77, 640
+    w = inputs.weights(N, K, cfg=16)
+    x = inputs.activations(M, K, cfg=16)
+    codes, qw, s, z = oracle_packed(w, 3)
+    ybuf = torch.full((M * N + 128,), 3.0, dtype=torch.float16, device=DEV)
+    laq.linear(to_dev(x), to_dev(qw.view(np.int32)), to_dev(s.view(np.float16)), to_dev(z), 3,
+               out=ybuf[:M * N].view(M, N))
+    torch.cuda.synchronize()
+    assert torch.all(ybuf[M * N:] == 3.0)
+    r = linear_check(ybuf[:M * N].view(M, N).cpu().numpy(), oracle.linear(x, codes, s, z))
+    assert r["ok"], r
+
+
+def test_two_streams():
+    say("two streams")
+    M, N, K = 2, 2048, 2560
+    w = inputs.weights(N, K, cfg=17)
+    x = inputs.activations(M, K, cfg=17)
+    codes, qw, s, z = oracle_packed(w, 3)
+    ref = gpu_linear(x, qw, s, z, 3)
+    xd, qd, sd, zd = to_dev(x), to_dev(qw.view(np.int32)), to_dev(s.view(np.float16)), to_dev(z)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for st in (s1, s2, s1, s2):
+        with torch.cuda.stream(st):
+            outs.append(laq.linear(xd, qd, sd, zd, 3))
+    torch.cuda.synchronize()
+    for o in outs:
+        assert np.array_equal(o.cpu().numpy(), ref)
+
+
+# ---------------------------------------------------------------------------
+# full-size shapes (the Qwen3-4B layer; Qwen3-32B projections on sampled rows)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("bits", [3, 4])
+def test_layer4b_full(bits):
+    """All seven Qwen3-4B projections at full size: GPU quantize bit-exact,
+    GPU linear (M = 1 and 16) on the GPU-quantized weights vs the oracle."""
+    for pi, (name, N, K) in enumerate(inputs.QWEN3_4B):
+        say("layer4b", bits, name, N, K)
+        w = inputs.weights(N, K, cfg=2, layer=0, proj=pi)
+        codes, qw, s, z = oracle_packed(w, bits)
+        gq, gs, gz = gpu_quantize(w, bits)
+        assert np.array_equal(gs, s) and np.array_equal(gz, z) and np.array_equal(gq, qw), name
+        for M in (1, 16):
+            x = inputs.activations(M, K, cfg=2, layer=0, slot=inputs.X_SLOT[name])
+            y = gpu_linear(x, gq, gs, gz, bits)
+            r = linear_check(y, oracle.linear(x, codes, s, z))
+            assert r["ok"], (name, M, r)
+
+
+def test_stack32b_sampled():
+    """Qwen3-32B projection shapes at full size on the GPU; the oracle checks
+    every output of sampled rows (quantize is per row, so sampling rows of
+    the weight matrix gives the same codes)."""
+    rng = np.random.default_rng(32)
+    for pi, (name, N, K) in enumerate(inputs.QWEN3_32B):
+        if name in ("k", "v", "up"):
+            continue
+        say("stack32b", name, N, K)
+        w = inputs.weights(N, K, cfg=5, layer=0, proj=pi)
+        rows = np.sort(rng.choice(N, 96, replace=False))
+        codes, qw, s, z = oracle_packed(np.ascontiguousarray(w[rows]), 3)
+        wd = to_dev(w)
+        q, sd, zd = laq.quantize(wd, 3)
+        del wd
+        torch.cuda.synchronize()
+        assert np.array_equal(sd[rows].cpu().numpy().view(np.uint16), s)
+        assert np.array_equal(zd[rows].cpu().numpy(), z)
+        assert np.array_equal(q[rows].cpu().numpy().view(np.uint32), qw)
+        for M in (1, 16):
+            x = inputs.activations(M, K, cfg=5, layer=0, slot=inputs.X_SLOT[name])
+            y = laq.linear(to_dev(x), q, sd, zd, 3)
+            torch.cuda.synchronize()
+            r = linear_check(y.cpu().numpy()[:, rows], oracle.linear(x, codes, s, z))
+            assert r["ok"], (name, M, r)
+        del q, sd, zd
+        torch.cuda.empty_cache()
