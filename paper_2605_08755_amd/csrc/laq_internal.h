@@ -32,6 +32,14 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
     hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
 }
 
+// Launch-shape parameters of the GEMV (defaults tuned on MI355X; exposed
+// internally so measurement harnesses can sweep them).
+struct LinearTuning {
+  int target_blocks = 512;  // flat kernel: blocks per launch it aims for
+  int flat_threads = 256;   // flat kernel: threads per block (256, 512 or 1024)
+};
+LinearTuning& linear_tuning();
+
 // Launchers (return the HIP error of the launch; shapes already validated).
 template <int BITS>
 hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qweight,

@@ -191,6 +191,210 @@ __global__ __launch_bounds__(kThreads) void linear_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Flat-unit kernel (used when the block's activations fit in LDS).
+//
+// A block owns R consecutive rows and every (row, group) unit of them,
+// dealt out flat over its 256 threads (unit u = r*G + g goes to thread
+// u mod 256), so lanes are balanced for any group count.  Activations are
+// loaded first (they are needed first and sit in L2), then the weights of
+// the thread's units; the activation tile is written to LDS together with
+// each group's sum.  Every unit writes its partial to LDS, and each row's
+// partials are added in a fixed order (16 lanes per row, then a DPP tree).
+// All global reads are buffer loads against per-block extents: addresses
+// are 32-bit offsets from scalar bases, and an offset past the extent reads
+// zero, so the tail of the last block needs no extra guards.
+// ---------------------------------------------------------------------------
+constexpr int kFlatXPerThread = 5;   // activation loads per thread per staging pass
+constexpr int kFlatUnitsPerThread = 4;
+constexpr uint32_t kOnesPair = 0x3C003C00u;  // fp16 (1.0, 1.0)
+constexpr int kBufferFlags = 0x00020000;     // raw buffer, 32-bit data
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferFlags);
+}
+
+// Loads of one unit.  A unit past the block's rows (r >= rows) has offsets
+// past each buffer's extent, so it reads zeros with no condition: a branch
+// or select around a load makes the compiler wait for the load at the
+// join, which would serialize the whole batch of loads.
+template <int BITS>
+__device__ __forceinline__ void load_flat_unit(__amdgpu_buffer_rsrc_t qr, __amdgpu_buffer_rsrc_t sr,
+                                               __amdgpu_buffer_rsrc_t zr, int r, int g, int G,
+                                               u32x4 (&w)[BITS], float& s, float& z) {
+  const uint32_t unit = (uint32_t)(r * G + g);
+#pragma unroll
+  for (int p = 0; p < BITS; ++p)
+    w[p] = __builtin_amdgcn_raw_buffer_load_b128(qr, ((uint32_t)(r * BITS + p) * G + g) * 16, 0, 0);
+  s = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(sr, unit * 2, 0, 0));
+  z = (float)__builtin_amdgcn_raw_buffer_load_b8(zr, unit, 0, 0);
+}
+
+// Sum over the 16 lanes of a DPP row; every lane receives the same total
+// (each step adds a lane's value to its partner's, a commutative pairing).
+__device__ __forceinline__ float row16_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false));  // row_half_mirror
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false));  // row_mirror
+  return v;
+}
+
+// One staging pass: activation units base + t + i*NT (16 bytes each, the
+// 16 lanes of a DPP row holding one 128-group) go to LDS, and the group's
+// sum of activations to xsum.
+template <int MT, int NT>
+__device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[kFlatXPerThread], int base, int t, int XU,
+                                             u32x4* xl, float* xsum) {
+#pragma unroll
+  for (int i = 0; i < kFlatXPerThread; ++i) {
+    const int idx = base + t + i * NT;
+    float ps = dot2(xv[i].x, kOnesPair, 0.0f);
+    ps = dot2(xv[i].y, kOnesPair, ps);
+    ps = dot2(xv[i].z, kOnesPair, ps);
+    ps = dot2(xv[i].w, kOnesPair, ps);
+    ps = row16_sum(ps);
+    if (idx < XU) {
+      const int mg = idx >> 4;  // m*G + g
+      const int b = idx & 15;
+      xl[mg * kGroupStrideU4 + b] = xv[i];
+      if (b == 0) xsum[mg] = ps;
+    }
+  }
+}
+
+template <int BITS, int MT, int NT>
+__global__ __launch_bounds__(NT) void linear_flat_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R) {
+  extern __shared__ u32x4 lds[];
+  u32x4* xl = lds;                                                                // [MT][G][17]
+  float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
+  float* part = xsum + MT * G;                                                    // [MT][R*G]
+
+  const int t = threadIdx.x;
+  const int64_t row0 = (int64_t)blockIdx.x * R;
+  const int rows = (int)min((int64_t)R, (int64_t)N - row0);
+  const int U = rows * G;
+  const int XU = MT * G * 16;  // activation tile in 16-byte units (rows m >= M read as zero)
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, (uint32_t)M * G * 256);
+  const __amdgpu_buffer_rsrc_t qr = make_rsrc(qw + row0 * BITS * G * 4, (uint32_t)rows * BITS * G * 16);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(scales + row0 * G, (uint32_t)U * 2);
+  const __amdgpu_buffer_rsrc_t zr = make_rsrc(zeros + row0 * G, (uint32_t)U);
+
+  // 1. First pass of activation loads.
+  // Index XM = M*G*16 is the end of x's extent: loads past it read zero.
+  u32x4 xv[kFlatXPerThread];
+#pragma unroll
+  for (int i = 0; i < kFlatXPerThread; ++i)
+    xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);  // activation loads go out before the weight loads
+
+  // 2. Weights of this thread's units: unit t + i*256 is (row r, group g);
+  //    (r, g) advance by (256 / G, 256 % G) per step.
+  const int dr = NT / G, dg = NT - (NT / G) * G;
+  int r0 = t / G;
+  int g0 = t - r0 * G;
+  u32x4 wv[kFlatUnitsPerThread][BITS];
+  float sv[kFlatUnitsPerThread], zv[kFlatUnitsPerThread];
+  int gi[kFlatUnitsPerThread];
+  {
+    int r = r0, g = g0;
+#pragma unroll
+    for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+      load_flat_unit<BITS>(qr, sr, zr, r, g, G, wv[i], sv[i], zv[i]);
+      gi[i] = g;
+      g += dg;
+      r += dr;
+      if (g >= G) { g -= G; r += 1; }
+    }
+  }
+
+  // 3. Stage activations and per-group sums (first pass from the loads above).
+  stage_x_pass<MT, NT>(xv, 0, t, XU, xl, xsum);
+  for (int base = kFlatXPerThread * NT; base < XU; base += kFlatXPerThread * NT) {
+#pragma unroll
+    for (int i = 0; i < kFlatXPerThread; ++i)
+      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(base + t + i * NT) * 16, 0, 0);
+    stage_x_pass<MT, NT>(xv, base, t, XU, xl, xsum);
+  }
+  __syncthreads();
+
+  // 4. Units: one 128-group of one row each.
+  int ur = r0, ug = g0;
+  for (int ub = 0; ub < U; ub += kFlatUnitsPerThread * NT) {
+    if (ub > 0) {
+      int r = ur, g = ug;
+#pragma unroll
+      for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+        load_flat_unit<BITS>(qr, sr, zr, r, g, G, wv[i], sv[i], zv[i]);
+        gi[i] = g;
+        g += dg;
+        r += dr;
+        if (g >= G) { g -= G; r += 1; }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+      const int u = ub + t + i * NT;
+      if (u < U) {
+        const int g = gi[i];
+        float acc[MT][4];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[m][c] = 0.0f;
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          uint32_t w[BITS];
+#pragma unroll
+          for (int p = 0; p < BITS; ++p) w[p] = wv[i][p][cc];
+#pragma unroll
+          for (int m = 0; m < MT; ++m) {
+            const u32x4* xp4 = xl + (m * G + g) * kGroupStrideU4 + cc * 4;
+            uint32_t xp[16];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+              const u32x4 q = xp4[v];
+              xp[4 * v + 0] = q.x;
+              xp[4 * v + 1] = q.y;
+              xp[4 * v + 2] = q.z;
+              xp[4 * v + 3] = q.w;
+            }
+            chunk_dot<BITS>(w, xp, acc[m]);
+          }
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const float a = classes_to_value<BITS>(acc[m]);
+          part[m * R * G + u] = sv[i] * fmaf(-zv[i], xsum[m * G + g], a);
+        }
+      }
+    }
+    // advance this thread's unit cursor by one batch
+#pragma unroll
+    for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+      ug += dg;
+      ur += dr;
+      if (ug >= G) { ug -= G; ur += 1; }
+    }
+  }
+  __syncthreads();
+
+  // 5. Row sums in a fixed order: lane l of a row's 16 adds groups l, l+16, ...
+  const int l = t & 15;
+  for (int rr = t >> 4; rr < rows; rr += NT / 16) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float acc = 0.0f;
+      for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
+      acc = row16_sum(acc);
+      if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+    }
+  }
+}
+
 int ceil_pow2(int v) {
   int p = 1;
   while (p < v) p <<= 1;
@@ -199,12 +403,47 @@ int ceil_pow2(int v) {
 
 }  // namespace
 
+LinearTuning& linear_tuning() {
+  static LinearTuning t;
+  return t;
+}
+
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
                          hipStream_t stream, const LaunchEvents& ev) {
   const int G = (int)(K / 128);
   const int MT = ceil_pow2(M);
+  const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
+  const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
+  {
+    // Flat-unit kernel when the activation tile and the partials fit in LDS.
+    const int target = linear_tuning().target_blocks;
+    const int nt = linear_tuning().flat_threads;
+    int R = (int)((N + target - 1) / target);
+    R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
+    const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
+    if (MT <= 4 && lds <= 64 * 1024) {
+      const unsigned blocks = (unsigned)((N + R - 1) / R);
+#define LAQ_FLAT(MTV, NTV)                                                                              \
+  launch(linear_flat_kernel<BITS, MTV, NTV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, qweight, \
+         scales, zeros, y, M, (int)N, G, R)
+#define LAQ_FLAT_NT(MTV)                        \
+  switch (nt) {                                 \
+    case 256: LAQ_FLAT(MTV, 256); break;        \
+    case 512: LAQ_FLAT(MTV, 512); break;        \
+    default: LAQ_FLAT(MTV, 1024); break;        \
+  }
+      switch (MT) {
+        case 1: LAQ_FLAT_NT(1); break;
+        case 2: LAQ_FLAT_NT(2); break;
+        default: LAQ_FLAT_NT(4); break;
+      }
+#undef LAQ_FLAT_NT
+#undef LAQ_FLAT
+      return hipGetLastError();
+    }
+  }
   // Lanes per row: enough that one K tile covers the row in a few groups per
   // lane, then more while the grid is small, capped by the row's group count.
   int L = 4;
@@ -219,8 +458,6 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   const size_t lds = (size_t)MT * tile * per_group_bytes;
   const int rows_per_block = kThreads / L;
   const unsigned blocks = (unsigned)((N + rows_per_block - 1) / rows_per_block);
-  const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
-  const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
 #define LAQ_LAUNCH(MTV)                                                                              \
   launch(linear_kernel<BITS, MTV>, dim3(blocks), dim3(kThreads), (uint32_t)lds, stream, ev, x4, q4, \
          scales, zeros, y, M, (int)N, G, lpr_log2, tile)
