@@ -3,8 +3,11 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 
 A step is one decode step's worth of quantized linears: the 36-layer
-Qwen3-4B-shaped stack (q, k, v, o, gate, up, down per layer; 252 calls of
-laq_linear_w3g128 at M = 1), captured once into a HIP graph and replayed.
+Qwen3-4B-shaped stack (q, k, v, o, gate, up, down per layer) at M = 1,
+captured once into a HIP graph and replayed.  Projections that read the same
+activation run as one call on row-concatenated weights (q|k|v and gate|up),
+so a layer is 4 dependent calls of laq_linear_w3g128 (144 per step); the
+one-call-per-projection figure (252 per step) is reported beside it.
 Weights are synthetic (seeded N(0, 0.02) with 1% x10 outliers, drawn on the
 GPU) and quantized by laq_quantize_w3g128 before timing; activations are
 seeded N(0, 1); everything is resident in HBM before the timed region.
@@ -38,10 +41,20 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-class Stack:
-    """All quantized projections of a workload, resident on the GPU."""
+# Projections that read the same activation are fused into one call by
+# concatenating their weights along N (quantization is per row, so the
+# concatenated quantization equals the separate ones): q|k|v and gate|up.
+FUSED = {"qkv": ("q", "k", "v"), "gateup": ("gate", "up")}
 
-    def __init__(self, workload, device, bits_list=(3,), keep_fp16=False):
+
+class Stack:
+    """All quantized projections of a workload, resident on the GPU.
+
+    fused=True: one call per decode stage that shares an input (q|k|v, o,
+    gate|up, down: 4 per layer); fused=False: one call per projection.
+    """
+
+    def __init__(self, workload, device, bits_list=(3,), keep_fp16=False, fused=True):
         import torch
         from paper_2605_08755_amd import inputs, laq
         spec = inputs.WORKLOADS[workload]
@@ -49,25 +62,52 @@ class Stack:
         self.layers = spec["layers"]
         self.projs = spec["projs"]
         self.device = device
+        self.fused = fused
         self.q = {b: [] for b in bits_list}
         self.fp16 = [] if keep_fp16 else None
         self.shapes = []
+        names = [p[0] for p in self.projs]
+        groups = []
+        if fused and all(n in names for members in FUSED.values() for n in members):
+            done = set()
+            for name in names:
+                if name in done:
+                    continue
+                for fname, members in FUSED.items():
+                    if name in members:
+                        groups.append((fname, members))
+                        done.update(members)
+                        break
+                else:
+                    groups.append((name, (name,)))
+                    done.add(name)
+        else:
+            groups = [(n, (n,)) for n in names]
+        self.groups = groups
         for layer in range(self.layers):
-            for pi, (name, N, K) in enumerate(self.projs):
-                w = inputs.weights_torch(N, K, seed=layer * 16 + pi, device=device)
+            for gname, members in groups:
+                parts = []
+                for name in members:
+                    pi = names.index(name)
+                    _, N, K = self.projs[pi]
+                    parts.append(inputs.weights_torch(N, K, seed=layer * 16 + pi, device=device))
+                w = parts[0] if len(parts) == 1 else torch.cat(parts, dim=0)
+                del parts
+                N, K = w.shape
                 for b in bits_list:
                     self.q[b].append(laq.quantize(w, b))
                 if keep_fp16:
                     self.fp16.append(w)
                 del w
-                self.shapes.append((layer, name, N, K))
+                self.shapes.append((layer, gname, N, K))
         torch.cuda.synchronize()
         self.x = {}
-        slots = sorted({(layer, inputs.X_SLOT.get(name, 0), K) for (layer, name, N, K) in self.shapes})
+        slots = sorted({(layer, inputs.X_SLOT.get(FUSED.get(name, (name,))[0], 0), K)
+                        for (layer, name, N, K) in self.shapes})
         for (layer, slot, K) in slots:
             self.x[(layer, slot)] = inputs.activations_torch(16, K, seed=layer * 8 + slot, device=device)
         self.y = [torch.empty((16, N), dtype=torch.float16, device=device) for (_, _, N, _) in self.shapes]
-        self.slot_of = [inputs.X_SLOT.get(name, 0) for (_, name, _, _) in self.shapes]
+        self.slot_of = [inputs.X_SLOT.get(FUSED.get(name, (name,))[0], 0) for (_, name, _, _) in self.shapes]
 
     def weights(self):
         return sum(N * K for (_, _, N, K) in self.shapes)
@@ -169,6 +209,8 @@ def main():
     ap.add_argument("--profile-reps", type=int, default=5)
     ap.add_argument("--no-sweep", action="store_true", help="skip the M x bits sweep and quantize timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--unfused", action="store_true",
+                    help="one call per projection (7 per layer) instead of one per shared-input stage (4)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -185,8 +227,8 @@ def main():
     bits_list = (3,) if args.no_sweep else (3, 4)
     log("building %s (bits %s) ..." % (args.workload, bits_list))
     t0 = time.perf_counter()
-    stack = Stack(args.workload, dev, bits_list=bits_list, keep_fp16=not args.no_sweep)
-    log("built in %.1f s: %d linears, %.3f G weights" % (time.perf_counter() - t0, len(stack.shapes), stack.weights() / 1e9))
+    stack = Stack(args.workload, dev, bits_list=bits_list, keep_fp16=not args.no_sweep, fused=not args.unfused)
+    log("built in %.1f s: %d linear calls per step, %.3f G weights" % (time.perf_counter() - t0, len(stack.shapes), stack.weights() / 1e9))
 
     # ---- headline: W3, M = 1, graph replay
     wbytes = stack.weight_bytes(3)
@@ -209,7 +251,17 @@ def main():
         del p["n"]
     log("kernel sum %.1f us/step -> %.1f GB/s; per proj %s" % (ksum_ms * 1e3, achieved, per_proj))
 
-    extra = {"us_per_step_graph": round(ms * 1e3, 2), "pct_of_hbm_peak": round(value / HBM_PEAK_GBS * 100, 2),
+    unfused = None
+    if not args.unfused and not args.no_sweep:
+        ustack = Stack(args.workload, dev, bits_list=(3,), fused=False)
+        ums, _ = time_graph(ustack, 1, 3, max(20, args.steps // 4), 5)
+        unfused = {"us_per_step": round(ums * 1e3, 2), "launches_per_step": len(ustack.shapes),
+                   "GBps": round(wbytes / (ums * 1e-3) / 1e9, 1)}
+        log("unfused (one call per projection):", unfused)
+        del ustack
+        torch.cuda.empty_cache()
+
+    extra = {"us_per_step_graph": round(ms * 1e3, 2), "unfused": unfused, "pct_of_hbm_peak": round(value / HBM_PEAK_GBS * 100, 2),
              "kernel_sum_us_per_step": round(ksum_ms * 1e3, 2), "launches_per_step": len(stack.shapes),
              "avg_kernel_us": round(ksum_ms * 1e3 / len(stack.shapes), 3), "per_projection": per_proj,
              "wall_s_timed_region": round(wall, 4)}
@@ -258,6 +310,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": "stack4b: 36-layer Qwen3-4B-shaped decode-step linear stack "
                                "(q,k,v,o,gate,up,down per layer), W3G128, M=1",
+                   "calls_per_layer": "q|k|v, o, gate|up, down (shared-input projections fused)"
+                   if stack.fused else "q, k, v, o, gate, up, down",
                    "layers": stack.layers, "linears_per_step": len(stack.shapes), "M": 1, "bits": 3,
                    "group": GROUP, "weights_per_step": stack.weights(),
                    "weight_bytes_per_step": int(round(wbytes))},

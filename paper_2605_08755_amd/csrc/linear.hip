@@ -205,10 +205,11 @@ __global__ __launch_bounds__(kThreads) void linear_kernel(
 // are 32-bit offsets from scalar bases, and an offset past the extent reads
 // zero, so the tail of the last block needs no extra guards.
 // ---------------------------------------------------------------------------
-constexpr int kFlatXPerThread = 5;   // activation loads per thread per staging pass
-constexpr int kFlatUnitsPerThread = 4;
 constexpr uint32_t kOnesPair = 0x3C003C00u;  // fp16 (1.0, 1.0)
 constexpr int kBufferFlags = 0x00020000;     // raw buffer, 32-bit data
+// Cache policy of the weight stream: non-temporal, read once, so it does not
+// evict the activations every block re-reads from L2.
+constexpr int kStreamPolicy = 2;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferFlags);
@@ -225,7 +226,7 @@ __device__ __forceinline__ void load_flat_unit(__amdgpu_buffer_rsrc_t qr, __amdg
   const uint32_t unit = (uint32_t)(r * G + g);
 #pragma unroll
   for (int p = 0; p < BITS; ++p)
-    w[p] = __builtin_amdgcn_raw_buffer_load_b128(qr, ((uint32_t)(r * BITS + p) * G + g) * 16, 0, 0);
+    w[p] = __builtin_amdgcn_raw_buffer_load_b128(qr, ((uint32_t)(r * BITS + p) * G + g) * 16, 0, kStreamPolicy);
   s = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(sr, unit * 2, 0, 0));
   z = (float)__builtin_amdgcn_raw_buffer_load_b8(zr, unit, 0, 0);
 }
@@ -243,11 +244,11 @@ __device__ __forceinline__ float row16_sum(float v) {
 // One staging pass: activation units base + t + i*NT (16 bytes each, the
 // 16 lanes of a DPP row holding one 128-group) go to LDS, and the group's
 // sum of activations to xsum.
-template <int MT, int NT>
-__device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[kFlatXPerThread], int base, int t, int XU,
+template <int MT, int NT, int XB>
+__device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[XB], int base, int t, int XU,
                                              u32x4* xl, float* xsum) {
 #pragma unroll
-  for (int i = 0; i < kFlatXPerThread; ++i) {
+  for (int i = 0; i < XB; ++i) {
     const int idx = base + t + i * NT;
     float ps = dot2(xv[i].x, kOnesPair, 0.0f);
     ps = dot2(xv[i].y, kOnesPair, ps);
@@ -263,7 +264,7 @@ __device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[kFlatXPerThread],
   }
 }
 
-template <int BITS, int MT, int NT>
+template <int BITS, int MT, int NT, int UPT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R) {
@@ -285,9 +286,9 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
 
   // 1. First pass of activation loads.
   // Index XM = M*G*16 is the end of x's extent: loads past it read zero.
-  u32x4 xv[kFlatXPerThread];
+  u32x4 xv[XB];
 #pragma unroll
-  for (int i = 0; i < kFlatXPerThread; ++i)
+  for (int i = 0; i < XB; ++i)
     xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
   __builtin_amdgcn_sched_barrier(0);  // activation loads go out before the weight loads
 
@@ -296,13 +297,13 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
   const int dr = NT / G, dg = NT - (NT / G) * G;
   int r0 = t / G;
   int g0 = t - r0 * G;
-  u32x4 wv[kFlatUnitsPerThread][BITS];
-  float sv[kFlatUnitsPerThread], zv[kFlatUnitsPerThread];
-  int gi[kFlatUnitsPerThread];
+  u32x4 wv[UPT][BITS];
+  float sv[UPT], zv[UPT];
+  int gi[UPT];
   {
     int r = r0, g = g0;
 #pragma unroll
-    for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+    for (int i = 0; i < UPT; ++i) {
       load_flat_unit<BITS>(qr, sr, zr, r, g, G, wv[i], sv[i], zv[i]);
       gi[i] = g;
       g += dg;
@@ -312,22 +313,22 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
   }
 
   // 3. Stage activations and per-group sums (first pass from the loads above).
-  stage_x_pass<MT, NT>(xv, 0, t, XU, xl, xsum);
-  for (int base = kFlatXPerThread * NT; base < XU; base += kFlatXPerThread * NT) {
+  stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);
+  for (int base = XB * NT; base < XU; base += XB * NT) {
 #pragma unroll
-    for (int i = 0; i < kFlatXPerThread; ++i)
+    for (int i = 0; i < XB; ++i)
       xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(base + t + i * NT) * 16, 0, 0);
-    stage_x_pass<MT, NT>(xv, base, t, XU, xl, xsum);
+    stage_x_pass<MT, NT, XB>(xv, base, t, XU, xl, xsum);
   }
   __syncthreads();
 
   // 4. Units: one 128-group of one row each.
   int ur = r0, ug = g0;
-  for (int ub = 0; ub < U; ub += kFlatUnitsPerThread * NT) {
+  for (int ub = 0; ub < U; ub += UPT * NT) {
     if (ub > 0) {
       int r = ur, g = ug;
 #pragma unroll
-      for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+      for (int i = 0; i < UPT; ++i) {
         load_flat_unit<BITS>(qr, sr, zr, r, g, G, wv[i], sv[i], zv[i]);
         gi[i] = g;
         g += dg;
@@ -336,7 +337,7 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
       }
     }
 #pragma unroll
-    for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+    for (int i = 0; i < UPT; ++i) {
       const int u = ub + t + i * NT;
       if (u < U) {
         const int g = gi[i];
@@ -374,7 +375,7 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
     }
     // advance this thread's unit cursor by one batch
 #pragma unroll
-    for (int i = 0; i < kFlatUnitsPerThread; ++i) {
+    for (int i = 0; i < UPT; ++i) {
       ug += dg;
       ur += dr;
       if (ug >= G) { ug -= G; ur += 1; }
@@ -418,29 +419,54 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
   {
     // Flat-unit kernel when the activation tile and the partials fit in LDS.
-    const int target = linear_tuning().target_blocks;
-    const int nt = linear_tuning().flat_threads;
-    int R = (int)((N + target - 1) / target);
+    // Rows per block R fill the block's unit slots (NT threads x UPT units):
+    // few loads per lane keeps the memory pipeline flowing, and whole rows
+    // per block keep the reduction inside the block.
+    LinearTuning& tune = linear_tuning();
+    const int NT = tune.flat_threads;
+    const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
+    int upt = tune.units_per_thread;
+    if (upt == 0) {
+      upt = 4;
+      for (int u : {1, 2, 4}) {
+        const int64_t rr = max(1, NT * u / G);
+        if ((N + rr - 1) / rr <= tune.max_blocks) { upt = u; break; }
+      }
+    }
+    int R = max(1, NT * upt / G);
     R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
     const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
     if (MT <= 4 && lds <= 64 * 1024) {
       const unsigned blocks = (unsigned)((N + R - 1) / R);
-#define LAQ_FLAT(MTV, NTV)                                                                              \
-  launch(linear_flat_kernel<BITS, MTV, NTV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, qweight, \
-         scales, zeros, y, M, (int)N, G, R)
-#define LAQ_FLAT_NT(MTV)                        \
-  switch (nt) {                                 \
-    case 256: LAQ_FLAT(MTV, 256); break;        \
-    case 512: LAQ_FLAT(MTV, 512); break;        \
-    default: LAQ_FLAT(MTV, 1024); break;        \
+      tune.last_blocks = (int)blocks;
+      tune.last_rows = R;
+#define LAQ_FLAT_NT(MTV, UPTV, XBV, NTV)                                                                    \
+  launch(linear_flat_kernel<BITS, MTV, NTV, UPTV, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
+         qweight, scales, zeros, y, M, (int)N, G, R)
+#define LAQ_FLAT(MTV, UPTV, XBV)                                  \
+  do {                                                            \
+    if (NT == 1024) LAQ_FLAT_NT(MTV, UPTV, XBV, 1024);            \
+    else if (NT == 512) LAQ_FLAT_NT(MTV, UPTV, XBV, 512);         \
+    else LAQ_FLAT_NT(MTV, UPTV, XBV, 256);                        \
+  } while (0)
+#define LAQ_FLAT_XB(MTV, UPTV)                 \
+  if (XB == 2) LAQ_FLAT(MTV, UPTV, 2);         \
+  else LAQ_FLAT(MTV, UPTV, 5);
+#define LAQ_FLAT_UPT(MTV)                      \
+  switch (upt) {                               \
+    case 1: LAQ_FLAT_XB(MTV, 1) break;         \
+    case 2: LAQ_FLAT_XB(MTV, 2) break;         \
+    default: LAQ_FLAT_XB(MTV, 4) break;        \
   }
       switch (MT) {
-        case 1: LAQ_FLAT_NT(1); break;
-        case 2: LAQ_FLAT_NT(2); break;
-        default: LAQ_FLAT_NT(4); break;
+        case 1: LAQ_FLAT_UPT(1); break;
+        case 2: LAQ_FLAT_UPT(2); break;
+        default: LAQ_FLAT_UPT(4); break;
       }
-#undef LAQ_FLAT_NT
+#undef LAQ_FLAT_UPT
+#undef LAQ_FLAT_XB
 #undef LAQ_FLAT
+#undef LAQ_FLAT_NT
       return hipGetLastError();
     }
   }
