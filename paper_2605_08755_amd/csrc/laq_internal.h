@@ -40,6 +40,7 @@ struct LinearTuning {
   int flat_threads = 256;    // flat kernel: threads per block (256, 512 or 1024)
   int last_blocks = 0;       // launch shape of the most recent flat launch (for harnesses)
   int last_rows = 0;
+  int mfma_min_m = 2;        // activation rows from which the matrix-core path is used
 };
 LinearTuning& linear_tuning();
 
@@ -48,6 +49,11 @@ template <int BITS>
 hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qweight,
                            uint16_t* scales, uint8_t* zeros, hipStream_t stream,
                            const LaunchEvents& ev);
+
+template <int BITS>
+hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
+                              const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
+                              hipStream_t stream, const LaunchEvents& ev);
 
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,

@@ -413,6 +413,8 @@ template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
                          hipStream_t stream, const LaunchEvents& ev) {
+  if (M >= linear_tuning().mfma_min_m)
+    return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev);
   const int G = (int)(K / 128);
   const int MT = ceil_pow2(M);
   const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
