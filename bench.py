@@ -32,6 +32,24 @@ HBM_PEAK_GBS = 8000.0
 GROUP = 128
 
 
+def measured_traffic():
+    """HBM bytes per GEMV launch from the committed rocprofv3 counter runs
+    (profiles/hbm_traffic.json), or None when the kernel source has changed
+    since those counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(os.path.join(ROOT, rec["kernel_source"]), "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    if digest != rec.get("kernel_source_sha256"):
+        return None
+    return rec
+
+
 def bytes_per_weight(bits):
     # codes + fp16 scale + uint8 zero per 128-group
     return bits / 8 + 2 / GROUP + 1 / GROUP
@@ -200,6 +218,26 @@ def cpu_baseline(budget_s=12.0):
             "us_per_step_equiv": round(dt * 36e6, 1)}
 
 
+def profile_run(args, dev):
+    """Workload for counter collection: a plain device copy of known size
+    (its FETCH_SIZE / WRITE_SIZE calibrate the counters) followed by eager
+    steps of the W3 M=1 stack (one dispatch per linear call)."""
+    import torch
+    nbytes = 256 << 20
+    a = torch.empty(nbytes // 2, dtype=torch.float16, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+    stack = Stack(args.workload, dev, bits_list=(3,), fused=not args.unfused)
+    for _ in range(args.steps):
+        stack.step(1, 3)
+    torch.cuda.synchronize()
+    print("profile run: copy 3 x %d bytes; %d steps x %d linear calls; %d weight bytes per step"
+          % (nbytes, args.steps, len(stack.shapes), int(stack.weight_bytes(3))), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -209,6 +247,9 @@ def main():
     ap.add_argument("--profile-reps", type=int, default=5)
     ap.add_argument("--no-sweep", action="store_true", help="skip the M x bits sweep and quantize timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-run", action="store_true",
+                    help="for rocprofv3: a 256 MiB device copy (counter calibration) and --steps eager "
+                         "W3 M=1 stack steps; prints a short summary instead of the JSON line")
     ap.add_argument("--unfused", action="store_true",
                     help="one call per projection (7 per layer) instead of one per shared-input stage (4)")
     args = ap.parse_args()
@@ -223,6 +264,10 @@ def main():
     laq.lib()  # fails loudly when liblaq.so is missing
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.profile_run:
+        profile_run(args, dev)
+        return
 
     bits_list = (3,) if args.no_sweep else (3, 4)
     log("building %s (bits %s) ..." % (args.workload, bits_list))
@@ -295,6 +340,7 @@ def main():
         extra["quantize_stack"] = dict(qd)
         log("quantize", extra["quantize_stack"])
 
+    traffic = measured_traffic()
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -316,8 +362,11 @@ def main():
                    "group": GROUP, "weights_per_step": stack.weights(),
                    "weight_bytes_per_step": int(round(wbytes))},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "linear_kernel<3,1> (W3G128 GEMV, M=1)"},
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None if traffic is None else traffic["hbm_bytes_per_launch"],
+                     "algorithmic_bytes_per_launch": int(round(wbytes / len(stack.shapes))),
+                     "avg_launch_us": round(ksum_ms * 1e3 / len(stack.shapes), 3),
+                     "kernel": "linear_flat_kernel<3,1,...> (W3G128 GEMV, M=1), all calls of the step"},
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(),
         "extra": extra,
     }
