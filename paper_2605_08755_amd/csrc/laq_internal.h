@@ -40,7 +40,8 @@ struct LinearTuning {
   int flat_threads = 256;    // flat kernel: threads per block (256, 512 or 1024)
   int last_blocks = 0;       // launch shape of the most recent flat launch (for harnesses)
   int last_rows = 0;
-  int mfma_min_m = 2;        // activation rows from which the matrix-core path is used
+  int mfma_min_m = 3;        // activation rows from which the matrix-core path may be used
+  int mfma_waves = 0;        // matrix-core kernel: waves per block (1..16); 0 = one per group quad
 };
 LinearTuning& linear_tuning();
 

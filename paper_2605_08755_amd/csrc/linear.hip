@@ -413,10 +413,13 @@ template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
                          hipStream_t stream, const LaunchEvents& ev) {
-  if (M >= linear_tuning().mfma_min_m)
-    return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev);
   const int G = (int)(K / 128);
   const int MT = ceil_pow2(M);
+  // Matrix cores from mfma_min_m rows on, except that the VALU kernel stays
+  // ahead up to 4 rows when rows are short (measured on MI355X: it re-reads
+  // the activations from LDS per unit, which costs more as rows get longer).
+  if (M >= linear_tuning().mfma_min_m && !(M <= 4 && G <= 24))
+    return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev);
   const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
   {
@@ -472,6 +475,9 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
       return hipGetLastError();
     }
   }
+  // Activation tile too large for the flat kernel's LDS: matrix cores for
+  // several rows, the K-tiled kernel below for one.
+  if (M >= 2) return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev);
   // Lanes per row: enough that one K tile covers the row in a few groups per
   // lane, then more while the grid is small, capped by the row's group count.
   int L = 4;

@@ -1,23 +1,21 @@
-// Skinny-GEMM path (M = 2..16 activation rows) on the matrix cores.
+// Skinny-GEMM path (several activation rows) on the matrix cores.
 //
 // y[m][n] = sum_g s[n][g] * sum_{k in g} x[m][k] * (q[n][k] - z[n][g])   (Eq. 1)
 //
 // One v_mfma_f32_16x16x32_f16 multiplies a 16 x 32 activation tile (rows m,
 // zero past M) by a 32 x 16 tile of exact (q - z) values of 16 weight rows.
-// Lane l of a wave owns weight row n = l % 16 of the current 16-row tile and
-// chunk q = l / 16 of the current 128-group, so the four chunks of a group
-// are spread over the four 16-lane quarters and every MFMA's 32-element K
-// window stays inside one group (one scale and zero point per row).  The
-// MFMA result fragment of lane l is column n = l % 16 (rows m = 4(l/16)..+3),
-// i.e. the lane's own weight row, so each lane scales its accumulator by its
-// own s[n][g] with no data exchange.
+// Lane l supplies weight row n = l % 16 and, within the 32-wide K window,
+// the 8 codes of chunk l / 16 of the current 128-group, so every window stays
+// inside one group (one scale and zero point per row).  The result fragment
+// of lane l is column n = l % 16 (rows m = 4(l/16)..+3), i.e. the lane's own
+// weight row, so each lane scales by its own row's s[n][g].
 //
 // Unpack to exact fp16 (q - z): OR-ing a 3-bit (or 4-bit) code field at
 // mantissa bits [p, p+b) with the bits of 2^(10-p) gives the fp16 value
 // 2^(10-p) + q exactly; one packed fp16 add of -(2^(10-p) + z) leaves q - z
 // exactly.  One v_and_or_b32 + one v_pk_add_f16 per two codes.
 //
-// The four waves of a block split the groups of the block's rows; their
+// The waves of a block split the groups of the block's 16 rows; their
 // partial sums are added in a fixed order through LDS (deterministic).
 #include "laq_internal.h"
 
@@ -28,7 +26,6 @@ namespace {
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kMfmaThreads = 256;  // 4 waves
 constexpr int kBufferFlagsM = 0x00020000;
 constexpr int kStreamPolicyM = 2;  // non-temporal weight stream
 
@@ -87,107 +84,125 @@ __device__ __forceinline__ half8_t frag(uint32_t a, uint32_t b, uint32_t c, uint
   return __builtin_bit_cast(half8_t, u32x4v{a, b, c, d});
 }
 
-// Loads of one (tile, group) for this lane: the chunk's BITS plane words,
-// the row's scale and zero point.  Rows past the block's extent read zeros.
-template <int BITS>
-struct TileLoad {
-  uint32_t w[BITS];
-  uint32_t s;
-  uint32_t z;
-};
+// An offset past every buffer extent: the load returns zero and moves no data.
+constexpr uint32_t kOffsetNone = 0x80000000u;
 
-template <int BITS, int TW>
-__global__ __launch_bounds__(kMfmaThreads) void linear_mfma_kernel(
+// 4 x 4 transpose across the four 16-lane quarters of a wave: on entry
+// register c of quarter j holds element (j, c); on exit register j of
+// quarter c holds it.  Two rounds of lane-half swaps (32 lanes, then 16).
+__device__ __forceinline__ void transpose_quarters(uint32_t& r0, uint32_t& r1, uint32_t& r2, uint32_t& r3) {
+  auto a = __builtin_amdgcn_permlane32_swap(r0, r2, false, false);
+  auto b = __builtin_amdgcn_permlane32_swap(r1, r3, false, false);
+  auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+  auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+  r0 = c[0];
+  r1 = c[1];
+  r2 = d[0];
+  r3 = d[1];
+}
+
+// Block: one tile of 16 weight rows and every group of them.  Work item of a
+// wave: the tile's four consecutive groups 4Q..4Q+3 (a "quad"); the W waves
+// of the block take quads wave, wave + W, ...
+//
+// Loads of a quad, lane (n = lane % 16, j = lane / 16): one 16-byte load per
+// plane of row n, group 4Q + j (four chunks), so each row of the tile reads
+// 64 contiguous bytes per plane; the scale and zero point of that (row,
+// group); and the activation fragments of the four groups (row m = n of x).
+// A quarter transpose then gives quarter q chunk q of every group of the
+// quad, the layout the matrix core wants (lane (n, q) supplies row n's codes
+// 32q .. 32q+31 of the group).  Slots past the last group read zeros.
+template <int BITS>
+__global__ __launch_bounds__(1024) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int K) {
-  __shared__ float red[4][TW][4][64];  // per-wave partial results, [wave][tile][r][lane]
+  extern __shared__ float red[];  // per-wave partial results, [wave][r][lane]
 
+  const int W = (int)(blockDim.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int nl = lane & 15;  // weight row within a tile / result column
-  const int q = lane >> 4;   // chunk of the group / activation row block
-  const int64_t row0 = (int64_t)blockIdx.x * (16 * TW);
-  const int rows = (int)min((int64_t)16 * TW, (int64_t)N - row0);
+  const int nl = lane & 15;  // weight row of the tile / activation row / result column
+  const int q = lane >> 4;   // load: group of the quad; compute: chunk of the group
+  const int64_t row0 = (int64_t)blockIdx.x * 16;
+  const int rows = (int)min((int64_t)16, (int64_t)N - row0);
   const int C = 4 * G;
+  const int nq = (G + 3) >> 2;
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
   const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * C, (uint32_t)rows * BITS * C * 4);
   const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
   const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
 
-  // this wave's share of the groups
-  const int g_begin = (G * wave) / 4;
-  const int g_end = (G * (wave + 1)) / 4;
+  float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
 
-  float4_t yacc[TW];
+  for (int Q = wave; Q < nq; Q += W) {
+    // 1. Loads.  Row n >= rows and x rows m >= M are past their extents.
+    const int gq = 4 * Q + q;
+    const bool okw = gq < G;
+    u32x4 wv[BITS];
 #pragma unroll
-  for (int t = 0; t < TW; ++t) yacc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
-
-  // activation fragment source: row m = lane % 16, bytes of chunk (4g + q)
-  const uint32_t xrow = (uint32_t)(lane & 15) * (uint32_t)K * 2;
-
-  auto load_group = [&](int g, u32x4 (&xa)[4], TileLoad<BITS> (&tl)[TW]) {
-    const uint32_t xo = xrow + (uint32_t)(128 * g + 32 * q) * 2;
+    for (int p = 0; p < BITS; ++p)
+      wv[p] = __builtin_amdgcn_raw_buffer_load_b128(
+          qr, okw ? (uint32_t)(((nl * BITS + p) * C + 4 * gq) * 4) : kOffsetNone, 0, kStreamPolicyM);
+    const uint32_t sraw = __builtin_amdgcn_raw_buffer_load_b16(sr, okw ? (uint32_t)(nl * G + gq) * 2 : kOffsetNone, 0, 0);
+    const uint32_t zraw = __builtin_amdgcn_raw_buffer_load_b8(zr, okw ? (uint32_t)(nl * G + gq) : kOffsetNone, 0, 0);
+    u32x4 xa[4][4];
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) xa[jj] = __builtin_amdgcn_raw_buffer_load_b128(xr, xo + 16 * jj, 0, 0);
+    for (int j = 0; j < 4; ++j) {
+      const int g = 4 * Q + j;
+      const uint32_t xo = g < G ? ((uint32_t)nl * (uint32_t)K + (uint32_t)(128 * g + 32 * q)) * 2 : kOffsetNone;
 #pragma unroll
-    for (int t = 0; t < TW; ++t) {
-      const uint32_t nloc = (uint32_t)(16 * t + nl);
-#pragma unroll
-      for (int p = 0; p < BITS; ++p)
-        tl[t].w[p] = __builtin_amdgcn_raw_buffer_load_b32(qr, ((nloc * BITS + p) * C + 4 * g + q) * 4, 0, kStreamPolicyM);
-      tl[t].s = __builtin_amdgcn_raw_buffer_load_b16(sr, (nloc * G + g) * 2, 0, 0);
-      tl[t].z = __builtin_amdgcn_raw_buffer_load_b8(zr, nloc * G + g, 0, 0);
+      for (int jj = 0; jj < 4; ++jj) xa[j][jj] = __builtin_amdgcn_raw_buffer_load_b128(xr, xo + 16 * jj, 0, 0);
     }
-  };
+    __builtin_amdgcn_sched_barrier(0);  // every load of the quad goes out before any compute
 
-  auto compute_group = [&](const u32x4 (&xc)[4], const TileLoad<BITS> (&tc)[TW]) {
+    // 2. Quarter transposes: plane words (chunk q of group 4Q + j now in
+    //    component j) and the four groups' scale | zero << 16 in every quarter.
+    uint32_t wt[BITS][4];
 #pragma unroll
-    for (int t = 0; t < TW; ++t) {
+    for (int p = 0; p < BITS; ++p) {
+      wt[p][0] = wv[p][0];
+      wt[p][1] = wv[p][1];
+      wt[p][2] = wv[p][2];
+      wt[p][3] = wv[p][3];
+      transpose_quarters(wt[p][0], wt[p][1], wt[p][2], wt[p][3]);
+    }
+    const uint32_t sz = sraw | (zraw << 16);
+    uint32_t szj[4] = {sz, sz, sz, sz};
+    transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
+
+    // 3. Per group: exact (q - z) pairs, four MFMAs, scale.
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t w[BITS];
+#pragma unroll
+      for (int p = 0; p < BITS; ++p) w[p] = wt[p][j];
       uint32_t pr[16];
-      unpack_chunk_exact<BITS>(tc[t].w, tc[t].z, pr);
+      unpack_chunk_exact<BITS>(w, szj[j] >> 16, pr);
       float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const half8_t a = __builtin_bit_cast(half8_t, xc[jj]);
+        const half8_t a = __builtin_bit_cast(half8_t, xa[j][jj]);
         const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
         c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
       }
-      const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)tc[t].s);
-      yacc[t] += s * c;
-    }
-  };
-
-  // Two-deep pipeline: the loads of the next group are in flight while the
-  // current one is unpacked and multiplied.
-  if (g_begin < g_end) {
-    u32x4 xa0[4], xa1[4];
-    TileLoad<BITS> tl0[TW], tl1[TW];
-    load_group(g_begin, xa0, tl0);
-    for (int g = g_begin; g < g_end; g += 2) {
-      if (g + 1 < g_end) load_group(g + 1, xa1, tl1);
-      compute_group(xa0, tl0);
-      if (g + 1 < g_end) {
-        if (g + 2 < g_end) load_group(g + 2, xa0, tl0);
-        compute_group(xa1, tl1);
-      }
+      const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[j] & 0xFFFFu));
+      yacc += s * c;
     }
   }
 
-  // fixed-order reduction of the four waves' partials
+  // 4. Fixed-order reduction of the W waves' partials.
 #pragma unroll
-  for (int t = 0; t < TW; ++t)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][t][r][lane] = yacc[t][r];
+  for (int r = 0; r < 4; ++r) red[(wave * 4 + r) * 64 + lane] = yacc[r];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < TW * 4 * 64; idx += kMfmaThreads) {
-    const int t = idx / 256;
-    const int r = (idx >> 6) & 3;
+  for (int idx = threadIdx.x; idx < 4 * 64; idx += blockDim.x) {
+    const int r = idx >> 6;
     const int ln = idx & 63;
-    const float v = ((red[0][t][r][ln] + red[1][t][r][ln]) + red[2][t][r][ln]) + red[3][t][r][ln];
+    float v = 0.0f;
+    for (int w = 0; w < W; ++w) v += red[(w * 4 + r) * 64 + ln];
     const int m = 4 * (ln >> 4) + r;
-    const int nloc = 16 * t + (ln & 15);
-    if (m < M && nloc < rows) y[(int64_t)m * N + row0 + nloc] = __builtin_bit_cast(uint16_t, (_Float16)v);
+    const int n = ln & 15;
+    if (m < M && n < rows) y[(int64_t)m * N + row0 + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
   }
 }
 
@@ -198,16 +213,15 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
                               const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
                               hipStream_t stream, const LaunchEvents& ev) {
   const int G = (int)(K / 128);
-  // Two tiles per wave when that still leaves a couple of blocks per CU.
-  const int tiles = (int)((N + 15) / 16);
-  const int TW = tiles >= 1024 ? 2 : 1;
-  const unsigned blocks = (unsigned)((N + 16 * TW - 1) / (16 * TW));
-  if (TW == 2)
-    launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(kMfmaThreads), 0, stream, ev, x, qweight, scales, zeros,
-           y, M, (int)N, G, (int)K);
-  else
-    launch(linear_mfma_kernel<BITS, 1>, dim3(blocks), dim3(kMfmaThreads), 0, stream, ev, x, qweight, scales, zeros,
-           y, M, (int)N, G, (int)K);
+  LinearTuning& tune = linear_tuning();
+  const int nq = (G + 3) / 4;
+  // One wave per quad of the row, at most 16 (longer rows loop).
+  const int W = tune.mfma_waves > 0 ? min(16, tune.mfma_waves) : min(16, nq);
+  const unsigned blocks = (unsigned)((N + 15) / 16);
+  tune.last_blocks = (int)blocks;
+  tune.last_rows = 16;
+  launch(linear_mfma_kernel<BITS>, dim3(blocks), dim3(64 * W), (uint32_t)W * 4 * 64 * 4, stream, ev, x, qweight,
+         scales, zeros, y, M, (int)N, G, (int)K);
   return hipGetLastError();
 }
 
