@@ -27,6 +27,8 @@ class Oracle:
         I64 = ctypes.c_int64
         L.laqo_quantize.argtypes = [P, I64, I64, ctypes.c_int, P, P, P]
         L.laqo_quantize.restype = None
+        L.laqo_codes_from_params.argtypes = [P, I64, I64, ctypes.c_int, P, P, P]
+        L.laqo_codes_from_params.restype = None
         L.laqo_pack.argtypes = [P, I64, I64, ctypes.c_int, P]
         L.laqo_pack.restype = ctypes.c_int
         L.laqo_unpack.argtypes = [P, I64, I64, ctypes.c_int, P]
@@ -75,6 +77,24 @@ class Oracle:
         zeros = np.empty((N, K // 128), np.uint8)
         self.lib.laqo_quantize(_p(w), N, K, bits, _p(codes), _p(scales), _p(zeros))
         return codes, scales, zeros
+
+    def codes_from_params(self, w, scales, zeros, bits=3):
+        """Eq. 1 with caller-supplied parameters: codes uint8 [N][K] from fp16
+        w [N][K], fp16 scales (bits or np.float16) [N][K/128] and uint8 zeros."""
+        w = np.ascontiguousarray(w)
+        if w.dtype == np.float16:
+            w = w.view(np.uint16)
+        scales = np.ascontiguousarray(scales)
+        if scales.dtype == np.float16:
+            scales = scales.view(np.uint16)
+        zeros = np.ascontiguousarray(zeros, dtype=np.uint8)
+        assert w.dtype == np.uint16 and w.ndim == 2 and scales.dtype == np.uint16
+        N, K = w.shape
+        assert K % 128 == 0 and K >= 128
+        assert scales.shape == (N, K // 128) and zeros.shape == (N, K // 128)
+        codes = np.empty((N, K), np.uint8)
+        self.lib.laqo_codes_from_params(_p(w), N, K, bits, _p(scales), _p(zeros), _p(codes))
+        return codes
 
     def pack(self, codes, bits=3):
         """codes uint8 [N][K] -> qweight uint32 [N][bits][K/32] (library layout)."""
@@ -136,6 +156,10 @@ def default() -> Oracle:
 
 def quantize(w, bits=3):
     return default().quantize(w, bits)
+
+
+def codes_from_params(w, scales, zeros, bits=3):
+    return default().codes_from_params(w, scales, zeros, bits)
 
 
 def pack(codes, bits=3):

@@ -18,7 +18,8 @@
  *    The paper learns s and z by QAT; this library computes them by
  *    round-to-nearest min-max over the group, with the range widened to
  *    contain 0 (lo <= 0 <= hi).  Arithmetic: IEEE fp32, round-half-to-even,
- *    true division, the scale rounded to fp16 before it is used.
+ *    true division, the scale rounded to fp16 before it is used.  The codes
+ *    of Eq. 1 for caller-supplied (e.g. trained) s and z are computed too.
  *  - Packing: 32 three-bit codes in three 32-bit words (App. G keeps this
  *    density of the GPTQ INT3 kernel), in this library's bit order; 4-bit
  *    codes eight per word.  The bit positions are computed here from the
@@ -137,6 +138,38 @@ void laqo_quantize(const uint16_t *w, int64_t N, int64_t K, int bits,
                 if (q > qmax) q = qmax;
                 codes[n * K + g * GROUP + i] = (uint8_t)q;
             }
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------
+ * Eq. 1 with given parameters: q = clip(round(w / s) + z, 0, 2^b - 1) for
+ * every weight, with s = scales[n][g] (binary16, finite and > 0) and
+ * z = zeros[n][g] (0 .. 2^b - 1) supplied by the caller, e.g. the scale and
+ * zero point that LAQuant's QAT learned.  Same arithmetic as above: fp32
+ * true division, round-half-to-even; the clip is taken on the real value,
+ * so quotients far outside the code range never reach an integer
+ * conversion.  A quotient that is not a number gives code 0.
+ * ------------------------------------------------------------------- */
+void laqo_codes_from_params(const uint16_t *w, int64_t N, int64_t K, int bits,
+                            const uint16_t *scales, const uint8_t *zeros,
+                            uint8_t *codes)
+{
+    const int64_t G = K / GROUP;
+    const float qmax = (float)((1 << bits) - 1);
+#pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t k = 0; k < K; ++k) {
+            const int64_t g = k / GROUP;
+            float s = laqo_f16_to_f32(scales[n * G + g]);
+            float z = (float)zeros[n * G + g];
+            float v = laqo_f16_to_f32(w[n * K + k]);
+            float u = rintf(v / s) + z;
+            if (!(u >= 0.0f))
+                u = 0.0f;
+            if (u > qmax)
+                u = qmax;
+            codes[n * K + k] = (uint8_t)u;
         }
     }
 }

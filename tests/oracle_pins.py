@@ -297,6 +297,64 @@ def pin_extremes(o, bits=3, seed=5):
 
 
 # ---------------------------------------------------------------------------
+# Eq. 1 with caller-supplied (s, z)
+# ---------------------------------------------------------------------------
+def pin_params_handworked(o):
+    """Worked by hand from Eq. 1 with s = 1/64 (exact in fp16) and given z:
+    w/s = 2.5 -> 2, 1.5 -> 2, -0.5 -> -0, 0.5 -> 0, 3.5 -> 4, -2.5 -> -2,
+    -1.5 -> -2, 4, -3, 0, 10, -10; plus z, then clipped to 0..qmax.
+    W3, z = 3: 5 5 3 3 7 1 1 7 0 3 7 0.  W4, z = 7: 9 9 7 7 11 5 5 11 4 7 15 0.
+    A second group with s = 1/2 and z = 0 maps w = 0.75 -> rint(1.5) = 2,
+    1.25 -> rint(2.5) = 2, -0.25 -> -0 -> 0, 3.0 -> 6 (W3) / 6 (W4)."""
+    ratios = [2.5, 1.5, -0.5, 0.5, 3.5, -2.5, -1.5, 4.0, -3.0, 0.0, 10.0, -10.0]
+    for bits, z0, exp in ((3, 3, [5, 5, 3, 3, 7, 1, 1, 7, 0, 3, 7, 0]),
+                          (4, 7, [9, 9, 7, 7, 11, 5, 5, 11, 4, 7, 15, 0])):
+        w = np.zeros((1, 256))
+        w[0, :len(ratios)] = np.array(ratios) / 64
+        w[0, 128:132] = [0.75, 1.25, -0.25, 3.0]
+        w = w.astype(np.float16)
+        scales = np.array([[py_float_to_half_bits(1 / 64), py_float_to_half_bits(0.5)]], np.uint16)
+        zeros = np.array([[z0, 0]], np.uint8)
+        c = o.codes_from_params(w, scales, zeros, bits)
+        assert c[0, :len(ratios)].tolist() == exp, (bits, c[0, :len(ratios)].tolist())
+        assert c[0, 128:132].tolist() == [2, 2, 0, 6], (bits, c[0, 128:132].tolist())
+        assert np.all(c[0, len(ratios):128] == z0) and np.all(c[0, 132:] == 0)
+
+
+def pin_params_exact(o, bits=3, seed=21):
+    """Random weights, random positive fp16 scales (subnormal to large) and
+    zero points: every code is clip(RNE(w/s) + z) of the exact rational
+    quotient, either neighbour allowed only within the fp32 quotient's
+    rounding of a tie."""
+    qmax = _levels(bits)
+    rng = np.random.default_rng(seed)
+    N, K = 12, 384
+    w = (rng.standard_normal((N, K)) * np.exp2(rng.integers(-12, 6, (N, 1)))).astype(np.float16)
+    w[0, :4] = [np.float16(65504), np.float16(-65504), np.float16(6e-8), np.float16(-0.0)]
+    exps = rng.integers(-24, 8, (N, K // 128))
+    sv = np.ldexp(1.0 + rng.integers(0, 1024, exps.shape) / 1024.0, exps)
+    scales = np.array([[py_float_to_half_bits(float(v)) for v in row] for row in sv], np.uint16)
+    scales[scales == 0] = 1
+    zeros = rng.integers(0, qmax + 1, (N, K // 128)).astype(np.uint8)
+    c = o.codes_from_params(w, scales, zeros, bits)
+    assert c.max() <= qmax
+    for n in range(N):
+        for k in range(K):
+            g = k // 128
+            v = Fraction(float(w[n, k])) / half_frac(int(scales[n, g])) + int(zeros[n, g])
+            margin = abs(v) * Fraction(2) ** -22 + Fraction(2) ** -40
+            assert int(c[n, k]) in _allowed_round(v, qmax, margin), (n, k, float(v), int(c[n, k]))
+
+
+def pin_params_match_quantize(o, bits=3, seed=22):
+    """Fed the scales and zero points that the min-max path chose, Eq. 1 gives
+    back that path's codes."""
+    w = inputs.weights(20, 512, cfg=93, layer=seed, proj=bits)
+    codes, scales, zeros = o.quantize(w, bits)
+    assert np.array_equal(o.codes_from_params(w, scales, zeros, bits), codes)
+
+
+# ---------------------------------------------------------------------------
 # packing pins
 # ---------------------------------------------------------------------------
 def _w3_words_spelled_out(q):
@@ -437,6 +495,13 @@ ALL_QUANT_PINS = (
     ("nearest_w4", lambda o: pin_nearest_level(o, 4)),
     ("permutation", pin_group_permutation),
     ("extremes", pin_extremes),
+)
+ALL_PARAMS_PINS = (
+    ("params_handworked", pin_params_handworked),
+    ("params_exact_w3", lambda o: pin_params_exact(o, 3)),
+    ("params_exact_w4", lambda o: pin_params_exact(o, 4)),
+    ("params_match_quantize_w3", lambda o: pin_params_match_quantize(o, 3)),
+    ("params_match_quantize_w4", lambda o: pin_params_match_quantize(o, 4)),
 )
 ALL_PACK_PINS = (("pack_fields", pin_pack_fields),)
 ALL_LINEAR_PINS = (

@@ -25,6 +25,11 @@ def test_quantize_pins(o, name, fn):
     fn(o)
 
 
+@pytest.mark.parametrize("name,fn", P.ALL_PARAMS_PINS, ids=[n for n, _ in P.ALL_PARAMS_PINS])
+def test_params_pins(o, name, fn):
+    fn(o)
+
+
 @pytest.mark.parametrize("name,fn", P.ALL_PACK_PINS, ids=[n for n, _ in P.ALL_PACK_PINS])
 def test_pack_pins(o, name, fn):
     fn(o)

@@ -34,13 +34,17 @@ MUTANTS = [
      "double xv = (double)laqo_f16_to_f32(x[(k % M) * K + (k / M) + m * 0]);"),
     ("linear_wrong_group_scale", "double s = (double)laqo_f16_to_f32(scales[n * G + g]);\n                int z",
      "double s = (double)laqo_f16_to_f32(scales[n * G + (G - 1 - g)]);\n                int z"),
+    ("params_floor_not_rint", "float u = rintf(v / s) + z;", "float u = floorf(v / s) + z;"),
+    ("params_zero_sign", "float u = rintf(v / s) + z;", "float u = rintf(v / s) - z;"),
+    ("params_first_group_scale", "float s = laqo_f16_to_f32(scales[n * G + g]);",
+     "float s = laqo_f16_to_f32(scales[n * G]);"),
     ("dequant_wrong_zero", "w_hat[n * K + k] = s * (double)((int)codes[n * K + k] - (int)zeros[n * G + g]);",
      "w_hat[n * K + k] = s * (double)((int)codes[n * K + k] - (int)zeros[n * G + 0]);"),
 ]
 
 
 def _all_pins():
-    return P.ALL_FP16_PINS + P.ALL_QUANT_PINS + P.ALL_PACK_PINS + P.ALL_LINEAR_PINS
+    return P.ALL_FP16_PINS + P.ALL_QUANT_PINS + P.ALL_PARAMS_PINS + P.ALL_PACK_PINS + P.ALL_LINEAR_PINS
 
 
 @pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
