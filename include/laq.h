@@ -11,6 +11,9 @@
  *   laq_quantize_w3g128 -- Eq. 1 (Sec. 2): q = clip(round(w/s) + z, 0, 7)
  *                          with round-to-nearest min-max s, z per 128-group,
  *                          packed 32 codes per three 32-bit words (App. G).
+ *   laq_pack_w3g128     -- Eq. 1 with caller-supplied s, z (for instance the
+ *                          scale and zero point LAQuant's QAT learned),
+ *                          packed the same way.
  *   laq_linear_w3g128   -- y = x * w_hat^T with w_hat = s * (q - z) (Eq. 1),
  *                          the fused dequantize GEMV / skinny GEMM of decode
  *                          (App. G describes the paper's INT3 GEMV).
@@ -123,6 +126,28 @@ laq_status laq_quantize_w3g128(const void *w, int64_t N, int64_t K,
                                void *stream);
 
 /*
+ * laq_pack_w3g128 -- Eq. 1 (Sec. 2) with caller-supplied parameters: the
+ * scale and zero point of every group are inputs (LAQuant learns them by
+ * QAT, Sec. 3; the deployed model is these codes plus those parameters).
+ *
+ * For row n, group g and every weight w of the group, in IEEE fp32 with
+ * round-half-to-even:
+ *   s = scales[n][g] (fp16, must be finite and > 0), z = zeros[n][g] (0..7)
+ *   q = clip(rint(w / s) + z, 0, 7)          (true division; the clip is on
+ *                                             the real value)
+ * and writes q packed exactly as laq_quantize_w3g128 does.  Fed the scales
+ * and zeros that laq_quantize_w3g128 wrote, it reproduces that call's
+ * qweight bit for bit.  scales and zeros are only read.
+ *
+ *   w        [in]  fp16 [N][K]
+ *   scales   [in]  fp16 [N][K/128]
+ *   zeros    [in]  uint8 [N][K/128]
+ *   qweight  [out] uint32 [N][3][K/32]
+ */
+laq_status laq_pack_w3g128(const void *w, const void *scales, const uint8_t *zeros,
+                           int64_t N, int64_t K, uint32_t *qweight, void *stream);
+
+/*
  * laq_linear_w3g128 -- y[m][n] = sum_k x[m][k] * s[n][g] * (q[n][k] - z[n][g]),
  * g = k/128: the dequantize-fused GEMV (M = 1) / skinny GEMM (M <= 16) of
  * decoding.  fp16 inputs, fp32 accumulation, one fp16 round-to-nearest-even
@@ -139,10 +164,13 @@ laq_status laq_linear_w3g128(const void *x, const uint32_t *qweight,
                              void *stream);
 
 /* W4G128 siblings: same contracts with 4-bit codes (0..15), s = (hi-lo)/15,
- * qweight uint32 [N][4][K/32] (N*K/2 bytes). */
+ * zero points 0..15, qweight uint32 [N][4][K/32] (N*K/2 bytes). */
 laq_status laq_quantize_w4g128(const void *w, int64_t N, int64_t K,
                                uint32_t *qweight, void *scales, uint8_t *zeros,
                                void *stream);
+
+laq_status laq_pack_w4g128(const void *w, const void *scales, const uint8_t *zeros,
+                           int64_t N, int64_t K, uint32_t *qweight, void *stream);
 
 laq_status laq_linear_w4g128(const void *x, const uint32_t *qweight,
                              const void *scales, const uint8_t *zeros,

@@ -62,6 +62,20 @@ laq_status quantize(const char* fn, const void* w, int64_t N, int64_t K, uint32_
 }
 
 template <int BITS>
+laq_status pack(const char* fn, const void* w, const void* scales, const uint8_t* zeros, int64_t N,
+                int64_t K, uint32_t* qweight, void* stream) {
+  const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
+  if (!w || !qweight || !scales || !zeros) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (!aligned(w, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "w and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales must be 2-byte aligned");
+  return hip_status(fn, laq::launch_pack<BITS>(static_cast<const uint16_t*>(w),
+                                               static_cast<const uint16_t*>(scales), zeros, N, K, qweight,
+                                               static_cast<hipStream_t>(stream), ev));
+}
+
+template <int BITS>
 laq_status linear(const char* fn, const void* x, const uint32_t* qweight, const void* scales,
                   const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {
   const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
@@ -111,6 +125,16 @@ laq_status laq_quantize_w3g128(const void* w, int64_t N, int64_t K, uint32_t* qw
 laq_status laq_quantize_w4g128(const void* w, int64_t N, int64_t K, uint32_t* qweight, void* scales,
                                uint8_t* zeros, void* stream) {
   return quantize<4>("laq_quantize_w4g128", w, N, K, qweight, scales, zeros, stream);
+}
+
+laq_status laq_pack_w3g128(const void* w, const void* scales, const uint8_t* zeros, int64_t N, int64_t K,
+                           uint32_t* qweight, void* stream) {
+  return pack<3>("laq_pack_w3g128", w, scales, zeros, N, K, qweight, stream);
+}
+
+laq_status laq_pack_w4g128(const void* w, const void* scales, const uint8_t* zeros, int64_t N, int64_t K,
+                           uint32_t* qweight, void* stream) {
+  return pack<4>("laq_pack_w4g128", w, scales, zeros, N, K, qweight, stream);
 }
 
 laq_status laq_linear_w3g128(const void* x, const uint32_t* qweight, const void* scales,

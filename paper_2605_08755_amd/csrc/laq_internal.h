@@ -52,6 +52,10 @@ hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qw
                            const LaunchEvents& ev);
 
 template <int BITS>
+hipError_t launch_pack(const uint16_t* w, const uint16_t* scales, const uint8_t* zeros, int64_t N,
+                       int64_t K, uint32_t* qweight, hipStream_t stream, const LaunchEvents& ev);
+
+template <int BITS>
 hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                               const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
                               hipStream_t stream, const LaunchEvents& ev);

@@ -284,19 +284,23 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
   const __amdgpu_buffer_rsrc_t sr = make_rsrc(scales + row0 * G, (uint32_t)U * 2);
   const __amdgpu_buffer_rsrc_t zr = make_rsrc(zeros + row0 * G, (uint32_t)U);
 
-  // 1. First pass of activation loads.
-  // Index XM = M*G*16 is the end of x's extent: loads past it read zero.
+  // Unit t + i*NT is (row r, group g); (r, g) advance by (NT / G, NT % G)
+  // per step.  Computed before any load so that no load waits on it.
+  const int dr = NT / G, dg = NT - (NT / G) * G;
+  const int r0 = t / G;
+  const int g0 = t - r0 * G;
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 1. First pass of activation loads (needed first: they are staged while
+  //    the weights stream in), then at once the weights of this thread's
+  //    units.  The scheduling barrier keeps the activation processing below
+  //    from being hoisted between the two batches of loads, which would make
+  //    the weight stream wait for an activation round trip.
+  //    Index XM = M*G*16 is the end of x's extent: loads past it read zero.
   u32x4 xv[XB];
 #pragma unroll
   for (int i = 0; i < XB; ++i)
     xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
-  __builtin_amdgcn_sched_barrier(0);  // activation loads go out before the weight loads
-
-  // 2. Weights of this thread's units: unit t + i*256 is (row r, group g);
-  //    (r, g) advance by (256 / G, 256 % G) per step.
-  const int dr = NT / G, dg = NT - (NT / G) * G;
-  int r0 = t / G;
-  int g0 = t - r0 * G;
   u32x4 wv[UPT][BITS];
   float sv[UPT], zv[UPT];
   int gi[UPT];
@@ -311,6 +315,7 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
       if (g >= G) { g -= G; r += 1; }
     }
   }
+  __builtin_amdgcn_sched_barrier(0);
 
   // 3. Stage activations and per-group sums (first pass from the loads above).
   stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);

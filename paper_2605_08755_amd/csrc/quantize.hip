@@ -9,6 +9,10 @@
 // exact in any order), every lane derives the same (s, z) with IEEE fp32
 // arithmetic, quantizes its 8 weights with true division and round-half-even,
 // and the 4 lanes of each 32-code chunk OR their bits into the plane words.
+//
+// The same kernel also packs with caller-supplied parameters (GIVEN): Eq. 1
+// with the scale and zero point read from memory (e.g. the ones LAQuant's
+// QAT learned) instead of the min-max ones.
 #include "laq_internal.h"
 
 namespace laq {
@@ -19,7 +23,7 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
 }
 
-template <int BITS>
+template <int BITS, bool GIVEN>
 __global__ __launch_bounds__(256) void quantize_kernel(const u32x4* __restrict__ w, int64_t n_groups,
                                                        int G, uint32_t* __restrict__ qweight,
                                                        uint16_t* __restrict__ scales,
@@ -35,26 +39,35 @@ __global__ __launch_bounds__(256) void quantize_kernel(const u32x4* __restrict__
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] = half_bits_to_float((words[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
 
-  // Group range, widened to contain 0.
-  float lo = 0.0f, hi = 0.0f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    lo = fminf(lo, v[e]);
-    hi = fmaxf(hi, v[e]);
-  }
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) {
-    lo = fminf(lo, __shfl_xor(lo, o, 16));
-    hi = fmaxf(hi, __shfl_xor(hi, o, 16));
-  }
-
   constexpr float qmax = (float)((1 << BITS) - 1);
-  const float s32 = (hi - lo) / qmax;  // IEEE division (no fast-math)
-  uint32_t s16 = __builtin_bit_cast(uint16_t, (_Float16)s32);  // round-to-nearest-even
-  if (s16 == 0) s16 = 1;                                       // 2^-24 when the range underflows
-  const float s = half_bits_to_float(s16);
-  const float z = fminf(fmaxf(rintf(-lo / s), 0.0f), qmax);
+  uint32_t s16;
+  float s, z;
+  if constexpr (GIVEN) {
+    s16 = scales[grp];
+    s = half_bits_to_float(s16);
+    z = (float)zeros[grp];
+  } else {
+    // Group range, widened to contain 0.
+    float lo = 0.0f, hi = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      lo = fminf(lo, v[e]);
+      hi = fmaxf(hi, v[e]);
+    }
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) {
+      lo = fminf(lo, __shfl_xor(lo, o, 16));
+      hi = fmaxf(hi, __shfl_xor(hi, o, 16));
+    }
+    const float s32 = (hi - lo) / qmax;  // IEEE division (no fast-math)
+    s16 = __builtin_bit_cast(uint16_t, (_Float16)s32);  // round-to-nearest-even
+    if (s16 == 0) s16 = 1;                              // 2^-24 when the range underflows
+    s = half_bits_to_float(s16);
+    z = fminf(fmaxf(rintf(-lo / s), 0.0f), qmax);
+  }
 
+  // Codes: the clip is taken on the real value (a quotient that is not a
+  // number gives 0), so no out-of-range value reaches the integer conversion.
   uint32_t q[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -108,7 +121,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const u32x4* __restrict__
       for (int p = 0; p < 3; ++p) qweight[(n * 3 + p) * C + c] = pw[p];
     }
   }
-  if (b == 0) {
+  if (!GIVEN && b == 0) {
     scales[grp] = (uint16_t)s16;
     zeros[grp] = (uint8_t)z;
   }
@@ -123,8 +136,21 @@ hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qw
   const int64_t G = K / 128;
   const int64_t n_groups = N * G;
   const int64_t blocks = (n_groups + 15) / 16;  // 16 groups per 256-thread block
-  launch(quantize_kernel<BITS>, dim3((unsigned)blocks), dim3(256), 0, stream, ev,
+  launch(quantize_kernel<BITS, false>, dim3((unsigned)blocks), dim3(256), 0, stream, ev,
          reinterpret_cast<const u32x4*>(w), n_groups, (int)G, qweight, scales, zeros);
+  return hipGetLastError();
+}
+
+template <int BITS>
+hipError_t launch_pack(const uint16_t* w, const uint16_t* scales, const uint8_t* zeros, int64_t N,
+                       int64_t K, uint32_t* qweight, hipStream_t stream, const LaunchEvents& ev) {
+  const int64_t G = K / 128;
+  const int64_t n_groups = N * G;
+  const int64_t blocks = (n_groups + 15) / 16;
+  // The GIVEN kernel only reads scales and zeros.
+  launch(quantize_kernel<BITS, true>, dim3((unsigned)blocks), dim3(256), 0, stream, ev,
+         reinterpret_cast<const u32x4*>(w), n_groups, (int)G, qweight, const_cast<uint16_t*>(scales),
+         const_cast<uint8_t*>(zeros));
   return hipGetLastError();
 }
 
@@ -132,5 +158,9 @@ template hipError_t launch_quantize<3>(const uint16_t*, int64_t, int64_t, uint32
                                        uint8_t*, hipStream_t, const LaunchEvents&);
 template hipError_t launch_quantize<4>(const uint16_t*, int64_t, int64_t, uint32_t*, uint16_t*,
                                        uint8_t*, hipStream_t, const LaunchEvents&);
+template hipError_t launch_pack<3>(const uint16_t*, const uint16_t*, const uint8_t*, int64_t, int64_t,
+                                   uint32_t*, hipStream_t, const LaunchEvents&);
+template hipError_t launch_pack<4>(const uint16_t*, const uint16_t*, const uint8_t*, int64_t, int64_t,
+                                   uint32_t*, hipStream_t, const LaunchEvents&);
 
 }  // namespace laq

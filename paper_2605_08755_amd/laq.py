@@ -21,8 +21,8 @@ MAX_M = 16
 GROUP = 128
 
 EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profile_next_launch",
-           "laq_quantize_w3g128", "laq_linear_w3g128",
-           "laq_quantize_w4g128", "laq_linear_w4g128")
+           "laq_quantize_w3g128", "laq_pack_w3g128", "laq_linear_w3g128",
+           "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128")
 
 _lib = None
 
@@ -53,6 +53,10 @@ def lib():
         for name in ("laq_quantize_w3g128", "laq_quantize_w4g128"):
             f = getattr(L, name)
             f.argtypes = [P, I64, I64, P, P, P, P]
+            f.restype = ctypes.c_int32
+        for name in ("laq_pack_w3g128", "laq_pack_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [P, P, P, I64, I64, P, P]
             f.restype = ctypes.c_int32
         for name in ("laq_linear_w3g128", "laq_linear_w4g128"):
             f = getattr(L, name)
@@ -109,6 +113,21 @@ def quantize(w, bits=3, out=None):
     return qweight, scales, zeros
 
 
+def pack(w, scales, zeros, bits=3, out=None):
+    """Eq. 1 with caller-supplied fp16 scales [N][K/128] and uint8 zero points
+    [N][K/128] (e.g. trained ones); returns qweight int32 [N][bits][K/32]."""
+    import torch
+    assert w.is_cuda and w.dtype == torch.float16 and w.dim() == 2 and w.is_contiguous()
+    N, K = w.shape
+    assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+    assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+    assert scales.is_contiguous() and zeros.is_contiguous()
+    qweight = torch.empty((N, bits, K // 32), dtype=torch.int32, device=w.device) if out is None else out
+    fn = lib().laq_pack_w3g128 if bits == 3 else lib().laq_pack_w4g128
+    _check(fn(_ptr(w), _ptr(scales), _ptr(zeros), N, K, _ptr(qweight), _stream(w.device)))
+    return qweight
+
+
 def linear(x, qweight, scales, zeros, bits=3, out=None):
     """y = x @ w_hat^T for fp16 x [M][K] (M <= 16) against packed weights."""
     import torch
@@ -126,6 +145,14 @@ def linear(x, qweight, scales, zeros, bits=3, out=None):
 
 def quantize_w3g128(w, out=None):
     return quantize(w, 3, out)
+
+
+def pack_w3g128(w, scales, zeros, out=None):
+    return pack(w, scales, zeros, 3, out)
+
+
+def pack_w4g128(w, scales, zeros, out=None):
+    return pack(w, scales, zeros, 4, out)
 
 
 def linear_w3g128(x, qweight, scales, zeros, out=None):

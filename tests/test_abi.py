@@ -47,6 +47,11 @@ def _quant(L, bits, w=FAKE, N=4, K=128, q=FAKE, s=FAKE, z=FAKE):
     return f(ctypes.c_void_p(w), N, K, ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z), None)
 
 
+def _pack(L, bits, w=FAKE, s=FAKE, z=FAKE, N=4, K=128, q=FAKE):
+    f = L.laq_pack_w3g128 if bits == 3 else L.laq_pack_w4g128
+    return f(ctypes.c_void_p(w), ctypes.c_void_p(s), ctypes.c_void_p(z), N, K, ctypes.c_void_p(q), None)
+
+
 def _lin(L, bits, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, M=1, N=4, K=128):
     f = L.laq_linear_w3g128 if bits == 3 else L.laq_linear_w4g128
     return f(ctypes.c_void_p(x), ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z),
@@ -70,6 +75,19 @@ def test_quantize_validation(L, bits):
     assert _quant(L, bits, q=FAKE + 4) == laq.LAQ_ERR_MISALIGNED
     assert _quant(L, bits, s=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
     assert b"laq_quantize" in L.laq_last_error()
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_pack_validation(L, bits):
+    for kw in ("w", "s", "z", "q"):
+        assert _pack(L, bits, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _pack(L, bits, N=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _pack(L, bits, K=96) == laq.LAQ_ERR_BAD_SHAPE
+    assert _pack(L, bits, K=1 << 25) == laq.LAQ_ERR_BAD_SHAPE
+    assert _pack(L, bits, w=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert _pack(L, bits, q=FAKE + 4) == laq.LAQ_ERR_MISALIGNED
+    assert _pack(L, bits, s=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_pack" in L.laq_last_error()
 
 
 @pytest.mark.parametrize("bits", [3, 4])

@@ -109,6 +109,79 @@ def test_quantize_canary():
 
 
 # ---------------------------------------------------------------------------
+# pack with caller-supplied scales and zero points (Eq. 1, trained parameters)
+# ---------------------------------------------------------------------------
+def random_params(N, K, bits, seed):
+    """Positive fp16 scales from the subnormal range to 2^7, zero points 0..qmax."""
+    rng = np.random.default_rng(seed)
+    G = K // 128
+    e = rng.integers(-24, 8, (N, G))
+    sv = np.ldexp(1.0 + rng.integers(0, 1024, (N, G)) / 1024.0, e).astype(np.float16)
+    sv[sv == 0] = np.float16(2.0 ** -24)
+    z = rng.integers(0, (1 << bits), (N, G)).astype(np.uint8)
+    return sv.view(np.uint16), z
+
+
+def gpu_pack(w16, s, z, bits):
+    qw = laq.pack(to_dev(w16), to_dev(s.view(np.float16)), to_dev(z), bits)
+    torch.cuda.synchronize()
+    return qw.cpu().numpy().view(np.uint32)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("N,K", QSHAPES)
+def test_pack_bitexact(bits, N, K):
+    say("pack", bits, N, K)
+    w = inputs.weights(N, K, cfg=13, layer=N, proj=K % 89)
+    s, z = random_params(N, K, bits, seed=N * 7 + K)
+    ref = oracle.pack(oracle.codes_from_params(w, s, z, bits), bits)
+    assert np.array_equal(gpu_pack(w, s, z, bits), ref)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_pack_reproduces_quantize(bits):
+    """Fed the parameters the min-max path wrote, pack gives its qweight."""
+    say("pack vs quantize", bits)
+    w = inputs.weights(129, 2560, cfg=14)
+    gq, gs, gz = gpu_quantize(w, bits)
+    assert np.array_equal(gpu_pack(w, gs, gz, bits), gq)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_pack_special(bits):
+    """Ties, clipping at both ends, extreme scales and weights."""
+    say("pack special", bits)
+    qmax = (1 << bits) - 1
+    K = 256
+    w = np.zeros((4, K))
+    w[0, :12] = np.array([2.5, 1.5, -0.5, 0.5, 3.5, -2.5, -1.5, 4.0, -3.0, 0.0, 10.0, -10.0]) / 64
+    w[1, :4] = [65504.0, -65504.0, 6e-8, -6e-8]
+    w[2, :] = np.linspace(-8, 8, K)
+    w[3, :] = -0.0
+    w = w.astype(np.float16)
+    s = np.array([[1 / 64, 0.5], [2.0 ** -24, 65504.0], [1.0, 2.0 ** -14], [0.25, 1.0]], np.float16).view(np.uint16)
+    z = np.array([[3 % (qmax + 1), 0], [qmax, 0], [0, qmax], [1, qmax]], np.uint8)
+    ref_codes = oracle.codes_from_params(w, s, z, bits)
+    assert np.array_equal(gpu_pack(w, s, z, bits), oracle.pack(ref_codes, bits))
+
+
+def test_pack_canary():
+    """pack writes only qweight; scales and zeros are left as they were."""
+    say("pack canary")
+    N, K = 21, 768
+    w = to_dev(inputs.weights(N, K, cfg=15))
+    s, z = random_params(N, K, 3, seed=5)
+    sd, zd = to_dev(s.view(np.float16)), to_dev(z)
+    s0, z0 = sd.clone(), zd.clone()
+    words = laq.packed_words(3, N, K)
+    qbuf = torch.full((words + 64,), 0x3C3C3C3C, dtype=torch.int32, device=DEV)
+    laq.pack(w, sd, zd, 3, out=qbuf[:words])
+    torch.cuda.synchronize()
+    assert torch.all(qbuf[words:] == 0x3C3C3C3C)
+    assert torch.equal(sd, s0) and torch.equal(zd, z0)
+
+
+# ---------------------------------------------------------------------------
 # linear
 # ---------------------------------------------------------------------------
 LSHAPES = [(1, 128), (17, 384), (64, 128), (300, 2560), (1024, 1024), (257, 4096), (96, 9728), (3, 25600)]
