@@ -168,6 +168,36 @@ def time_graph(stack, M, bits, steps, warmup):
     return ms, wall
 
 
+def time_fp16_graph(stack, M, steps, warmup):
+    """The same step with the fp16 weights through torch's dense GEMM
+    (hipBLASLt): the unquantized reference for the quantized speed-up."""
+    import torch
+
+    def step():
+        for i, (layer, name, N, K) in enumerate(stack.shapes):
+            torch.mm(stack.x[(layer, stack.slot_of[i])][:M], stack.fp16[i].t(), out=stack.y[i][:M])
+
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    step()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        step()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    del g
+    return ms
+
+
 def kernel_durations(stack, M, bits, reps):
     """Per-launch kernel durations (ms) from events recorded at kernel start/end."""
     import torch
@@ -337,8 +367,28 @@ def main():
             qms = e0.elapsed_time(e1)
             qbytes = stack.weights() * (2 + bytes_per_weight(bits))
             qd.append(("w%d" % bits, {"ms": round(qms, 3), "GBps": round(qbytes / (qms * 1e-3) / 1e9, 1)}))
+        # pack with given parameters (the ones quantize just wrote), W3
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        outs = stack.q[3]
+        e0.record()
+        for i, w in enumerate(stack.fp16):
+            laq.pack(w, outs[i][1], outs[i][2], 3, out=outs[i][0])
+        e1.record()
+        torch.cuda.synchronize()
+        pms = e0.elapsed_time(e1)
+        qd.append(("pack_w3", {"ms": round(pms, 3), "GBps": round(stack.weights() * (2 + bytes_per_weight(3)) / (pms * 1e-3) / 1e9, 1)}))
         extra["quantize_stack"] = dict(qd)
         log("quantize", extra["quantize_stack"])
+        # unquantized reference: fp16 weights through torch's dense GEMM
+        fp = {}
+        for M in (1, 16):
+            fms = time_fp16_graph(stack, M, max(20, args.steps // 4), 5)
+            w3 = sweep["w3_m%d" % M]["us"]
+            fp["m%d" % M] = {"us": round(fms * 1e3, 2), "GBps": round(stack.weights() * 2 / (fms * 1e-3) / 1e9, 1),
+                             "w3_speedup": round(fms * 1e3 / w3, 3)}
+        extra["fp16_dense_torch"] = fp
+        log("fp16 dense (torch.mm):", fp)
 
     traffic = measured_traffic()
     out = {
