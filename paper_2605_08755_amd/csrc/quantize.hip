@@ -3,11 +3,12 @@
 // into the plane layout of include/laq.h (32 codes in three 32-bit words for
 // W3, as App. G keeps; eight 4-bit codes per word for W4).
 //
-// Mapping: 16 lanes per group, each lane owns 8 consecutive weights (one
-// 16-byte load; a group is 256 contiguous bytes, so a wave reads 1 KB
-// contiguous).  The group range is reduced across the 16 lanes (min/max are
-// exact in any order), every lane derives the same (s, z) with IEEE fp32
-// arithmetic, quantizes its 8 weights with true division and round-half-even,
+// Mapping: 16 lanes per group (one DPP row), each lane owns 8 consecutive
+// weights (one 16-byte load; a group is 256 contiguous bytes, so a wave reads
+// 1 KB contiguous).  The group range is reduced across the 16 lanes with DPP
+// (min/max are exact in any order), every lane derives the same (s, z) with IEEE fp32
+// arithmetic, quantizes its 8 weights with the IEEE quotient (formed from a
+// reciprocal and two fused multiply-adds, see below) and round-half-even,
 // and the 4 lanes of each 32-code chunk OR their bits into the plane words.
 //
 // The same kernel also packs with caller-supplied parameters (GIVEN): Eq. 1
@@ -21,6 +22,26 @@ namespace {
 
 __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL>
+__device__ __forceinline__ void minmax_step(float& lo, float& hi) {
+  lo = fminf(lo, dpp<CTRL>(lo));
+  hi = fmaxf(hi, dpp<CTRL>(hi));
+}
+
+// Minimum and maximum over the 16 lanes of a DPP row (a group's lanes);
+// every lane receives both.  Exact in any order.
+__device__ __forceinline__ void row16_minmax(float& lo, float& hi) {
+  minmax_step<0xB1>(lo, hi);   // quad_perm [1,0,3,2]
+  minmax_step<0x4E>(lo, hi);   // quad_perm [2,3,0,1]
+  minmax_step<0x141>(lo, hi);  // row_half_mirror
+  minmax_step<0x140>(lo, hi);  // row_mirror
 }
 
 template <int BITS, bool GIVEN>
@@ -54,11 +75,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const u32x4* __restrict__
       lo = fminf(lo, v[e]);
       hi = fmaxf(hi, v[e]);
     }
-#pragma unroll
-    for (int o = 8; o >= 1; o >>= 1) {
-      lo = fminf(lo, __shfl_xor(lo, o, 16));
-      hi = fmaxf(hi, __shfl_xor(hi, o, 16));
-    }
+    row16_minmax(lo, hi);
     const float s32 = (hi - lo) / qmax;  // IEEE division (no fast-math)
     s16 = __builtin_bit_cast(uint16_t, (_Float16)s32);  // round-to-nearest-even
     if (s16 == 0) s16 = 1;                              // 2^-24 when the range underflows
@@ -68,15 +85,46 @@ __global__ __launch_bounds__(256) void quantize_kernel(const u32x4* __restrict__
 
   // Codes: the clip is taken on the real value (a quotient that is not a
   // number gives 0), so no out-of-range value reaches the integer conversion.
+  //
+  // The quotient v / s is formed without a per-weight division: with
+  // y = RN(1/s) (one IEEE division per group), q = RN(v*y), r = v - q*s
+  // (exact, fused) and q' = RN(q + r*y) (fused), q' equals the IEEE binary32
+  // quotient RN(v/s) for every finite fp16 v and every finite positive fp16
+  // s -- checked exhaustively over all 2.0e9 such pairs
+  // (tests/native/fp16_quotient_check.c).  The min-max scale is always in
+  // that domain; a caller-supplied scale outside it (zero, infinite or not
+  // a number) takes the true division.
   uint32_t q[8];
+  if (!GIVEN || (s > 0.0f && s <= 65504.0f)) {
+    const float y = 1.0f / s;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float t = fminf(fmaxf(rintf(v[e] / s) + z, 0.0f), qmax);
-    q[e] = (uint32_t)t;
+    for (int e = 0; e < 8; ++e) {
+      const float q0 = v[e] * y;
+      const float r = fmaf(-q0, s, v[e]);
+      const float qt = fmaf(r, y, q0);
+      q[e] = (uint32_t)fminf(fmaxf(rintf(qt) + z, 0.0f), qmax);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[e] = (uint32_t)fminf(fmaxf(rintf(v[e] / s) + z, 0.0f), qmax);
   }
 
-  const int64_t n = grp / G;
-  const int g = (int)(grp - n * G);
+  // (row, group) of this lane: the block's first group splits on the scalar
+  // unit; a lane's group is at most 15 further, i.e. one row wrap when G >= 16.
+  const int64_t base = (int64_t)blockIdx.x * 16;
+  const int64_t n0 = base / G;
+  const int g0 = (int)(base - n0 * G);
+  int g = g0 + (int)(threadIdx.x >> 4);
+  int64_t n = n0;
+  if (G >= 16) {
+    if (g >= G) {
+      g -= G;
+      n += 1;
+    }
+  } else {
+    n += g / G;
+    g = g % G;
+  }
   const int chunk = b >> 2;  // 32-code chunk of the group this lane belongs to
   const int sub = b & 3;     // which 8 codes of the chunk (codes 8*sub .. 8*sub+7)
   const int64_t C = 4 * (int64_t)G;
@@ -90,36 +138,35 @@ __global__ __launch_bounds__(256) void quantize_kernel(const u32x4* __restrict__
     for (int e = 0; e < 8; ++e) word |= q[e] << (((e & 1) << 4) + ((e >> 1) << 2));
     qweight[(n * 4 + sub) * C + c] = word;
   } else {
-    // Three planes, each holding ten codes in five 3-bit fields per 16-bit
-    // half; the last two codes of the chunk are spread one bit per plane.
-    uint32_t pw[3] = {0u, 0u, 0u};
+    // The chunk's 32 codes in natural order (code i at bits 3i of a 96-bit
+    // string W2:W1:W0), assembled in every lane of the chunk's quad from the
+    // four lanes' 24-bit pieces.  Lane `sub` < 3 then builds plane `sub`:
+    // codes 10*sub .. 10*sub+9 are the 30 bits starting at bit 30*sub, placed
+    // into the five 3-bit fields of each 16-bit half, plus bit `sub` of codes
+    // 30 and 31 at bits 9 and 25.
+    uint32_t nat = 0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int i = 8 * sub + e;  // code index in the chunk
-      if (i < 30) {
-        const int plane = i / 10;
-        const int r = i - 10 * plane;
-        const int field = r >> 1;
-        const int shift = ((r & 1) << 4) + 3 * field + (field >= 3 ? 1 : 0);
-        const uint32_t bits = q[e] << shift;
-        pw[0] |= plane == 0 ? bits : 0u;
-        pw[1] |= plane == 1 ? bits : 0u;
-        pw[2] |= plane == 2 ? bits : 0u;
-      } else {
-        const int pos = (i == 30) ? 9 : 25;
+    for (int e = 0; e < 8; ++e) nat |= q[e] << (3 * e);
+    const uint32_t n0w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)nat, 0x00, 0xF, 0xF, false);  // quad_perm [0,0,0,0]
+    const uint32_t n1w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)nat, 0x55, 0xF, 0xF, false);  // quad_perm [1,1,1,1]
+    const uint32_t n2w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)nat, 0xAA, 0xF, 0xF, false);  // quad_perm [2,2,2,2]
+    const uint32_t n3w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)nat, 0xFF, 0xF, 0xF, false);  // quad_perm [3,3,3,3]
+    const uint32_t W0 = n0w | (n1w << 24);
+    const uint32_t W1 = (n1w >> 8) | (n2w << 16);
+    const uint32_t W2 = (n2w >> 16) | (n3w << 8);
+    const uint32_t win1 = __builtin_amdgcn_alignbit(W1, W0, 30);  // bits 30..61
+    const uint32_t win2 = __builtin_amdgcn_alignbit(W2, W1, 28);  // bits 60..91
+    const uint32_t win = sub == 0 ? W0 : (sub == 1 ? win1 : win2);
+    uint32_t pw = 0;
 #pragma unroll
-        for (int p = 0; p < 3; ++p) pw[p] |= ((q[e] >> p) & 1u) << pos;
-      }
+    for (int j = 0; j < 10; ++j) {
+      const int field = j >> 1;
+      const int shift = ((j & 1) << 4) + 3 * field + (field >= 3 ? 1 : 0);
+      pw |= ((win >> (3 * j)) & 7u) << shift;
     }
-#pragma unroll
-    for (int p = 0; p < 3; ++p) {
-      pw[p] |= __shfl_xor(pw[p], 1, 4);
-      pw[p] |= __shfl_xor(pw[p], 2, 4);
-    }
-    if (sub == 0) {
-#pragma unroll
-      for (int p = 0; p < 3; ++p) qweight[(n * 3 + p) * C + c] = pw[p];
-    }
+    const uint32_t spare = W2 >> (26 + sub);  // bit 0: bit `sub` of code 30; bit 3: of code 31
+    pw |= ((spare & 1u) << 9) | (((spare >> 3) & 1u) << 25);
+    if (sub < 3) qweight[(n * 3 + sub) * C + c] = pw;
   }
   if (!GIVEN && b == 0) {
     scales[grp] = (uint16_t)s16;
