@@ -198,6 +198,39 @@ def time_fp16_graph(stack, M, steps, warmup):
     return ms
 
 
+def stack32b_extra(dev, steps):
+    """The 64-layer Qwen3-32B-shaped stack: W3 decode-step time at M = 1 and
+    16, and quantize throughput over all of its fp16 weights."""
+    import torch
+    from paper_2605_08755_amd import laq
+    t0 = time.perf_counter()
+    st = Stack("stack32b", dev, bits_list=(3,), keep_fp16=True, fused=True)
+    log("stack32b built in %.1f s: %d calls per step, %.2f G weights"
+        % (time.perf_counter() - t0, len(st.shapes), st.weights() / 1e9))
+    wb = st.weight_bytes(3)
+    out = {"layers": st.layers, "weights_per_step": st.weights(), "weight_bytes_per_step": int(round(wb)),
+           "linears_per_step": len(st.shapes)}
+    for M in (1, 16):
+        ms, _ = time_graph(st, M, 3, steps, 5)
+        gbs = wb / (ms * 1e-3) / 1e9
+        out["w3_m%d" % M] = {"us": round(ms * 1e3, 1), "GBps": round(gbs, 1),
+                             "pct_of_hbm_peak": round(gbs / HBM_PEAK_GBS * 100, 2)}
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i, w in enumerate(st.fp16):
+        laq.quantize(w, 3, out=st.q[3][i])
+    e1.record()
+    torch.cuda.synchronize()
+    qms = e0.elapsed_time(e1)
+    out["quantize_w3"] = {"ms": round(qms, 3),
+                          "GBps": round(st.weights() * (2 + bytes_per_weight(3)) / (qms * 1e-3) / 1e9, 1)}
+    log("stack32b:", out)
+    del st
+    torch.cuda.empty_cache()
+    return out
+
+
 def kernel_durations(stack, M, bits, reps):
     """Per-launch kernel durations (ms) from events recorded at kernel start/end."""
     import torch
@@ -389,6 +422,14 @@ def main():
                              "w3_speedup": round(fms * 1e3 / w3, 3)}
         extra["fp16_dense_torch"] = fp
         log("fp16 dense (torch.mm):", fp)
+
+    if not args.no_sweep:
+        stack.fp16 = None  # free the 4B stack's tensors; its shapes stay for the report
+        stack.q = None
+        stack.x = None
+        stack.y = None
+        torch.cuda.empty_cache()
+        extra["stack32b"] = stack32b_extra(dev, max(10, args.steps // 10))
 
     traffic = measured_traffic()
     out = {

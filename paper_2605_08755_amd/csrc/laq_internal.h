@@ -37,7 +37,7 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
 struct LinearTuning {
   int max_blocks = 1 << 20;  // flat kernel: fewest units per thread whose grid stays within this
   int units_per_thread = 0;  // flat kernel: 1, 2 or 4; 0 = chosen from max_blocks
-  int flat_threads = 256;    // flat kernel: threads per block (256, 512 or 1024)
+  int flat_threads = 0;      // flat kernel: threads per block (256, 512 or 1024); 0 = chosen from K
   int last_blocks = 0;       // launch shape of the most recent flat launch (for harnesses)
   int last_rows = 0;
   int mfma_min_m = 3;        // activation rows from which the matrix-core path may be used

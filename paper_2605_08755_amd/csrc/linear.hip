@@ -433,7 +433,9 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     // few loads per lane keeps the memory pipeline flowing, and whole rows
     // per block keep the reduction inside the block.
     LinearTuning& tune = linear_tuning();
-    const int NT = tune.flat_threads;
+    // Threads per block: every block stages the whole activation row, so
+    // longer rows want more rows per block (about 8 or more) to amortize it.
+    const int NT = tune.flat_threads > 0 ? tune.flat_threads : (G <= 32 ? 256 : (G <= 64 ? 512 : 1024));
     const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
     int upt = tune.units_per_thread;
     if (upt == 0) {
