@@ -343,3 +343,24 @@ def test_stack32b_sampled():
             assert r["ok"], (name, M, r)
         del q, sd, zd
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_max_k(bits):
+    """The largest K the ABI accepts (2^24): quantize and pack bit-exact, and
+    the linear at M = 1 (K-tiled kernel: the activation row exceeds LDS), 2
+    and 16 (matrix cores, many quad batches per wave) against the oracle."""
+    K = 1 << 24
+    N = 3
+    say("max K", bits, N, K)
+    rng = np.random.default_rng(77)
+    w = (rng.standard_normal((N, K), dtype=np.float32) * 0.02).astype(np.float16)
+    codes, qw, s, z = oracle_packed(w, bits)
+    gq, gs, gz = gpu_quantize(w, bits)
+    assert np.array_equal(gs, s) and np.array_equal(gz, z) and np.array_equal(gq, qw)
+    assert np.array_equal(gpu_pack(w, s, z, bits), qw)
+    for M in (1, 2, 16):
+        x = rng.standard_normal((M, K), dtype=np.float32).astype(np.float16)
+        y = gpu_linear(x, qw, s, z, bits)
+        r = linear_check(y, oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
