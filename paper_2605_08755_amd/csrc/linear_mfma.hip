@@ -101,30 +101,31 @@ __device__ __forceinline__ void transpose_quarters(uint32_t& r0, uint32_t& r1, u
   r3 = d[1];
 }
 
-// Block: one tile of 16 weight rows and every group of them.  Work item of a
-// wave: the tile's four consecutive groups 4Q..4Q+3 (a "quad"); the W waves
-// of the block take quads wave, wave + W, ...
+// Block: TW tiles of 16 weight rows and every group of them.  Work item of a
+// wave: the four consecutive groups 4Q..4Q+3 (a "quad") of all TW tiles; the
+// W waves of the block take quads wave, wave + W, ...  The activation
+// fragments of a quad are loaded once per wave and serve all TW tiles.
 //
-// Loads of a quad, lane (n = lane % 16, j = lane / 16): one 16-byte load per
-// plane of row n, group 4Q + j (four chunks), so each row of the tile reads
-// 64 contiguous bytes per plane; the scale and zero point of that (row,
-// group); and the activation fragments of the four groups (row m = n of x).
-// A quarter transpose then gives quarter q chunk q of every group of the
-// quad, the layout the matrix core wants (lane (n, q) supplies row n's codes
-// 32q .. 32q+31 of the group).  Slots past the last group read zeros.
-template <int BITS>
-__global__ __launch_bounds__(1024) void linear_mfma_kernel(
+// Loads of a quad, lane (n = lane % 16, j = lane / 16): per tile, one 16-byte
+// load per plane of row n, group 4Q + j (four chunks), so each row of a tile
+// reads 64 contiguous bytes per plane, and the scale and zero point of that
+// (row, group); once, the activation fragments of the four groups (row m = n
+// of x).  A quarter transpose then gives quarter q chunk q of every group of
+// the quad, the layout the matrix core wants (lane (n, q) supplies row n's
+// codes 32q .. 32q+31 of the group).  Slots past the last group read zeros.
+template <int BITS, int TW>
+__global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int K) {
-  extern __shared__ float red[];  // per-wave partial results, [wave][r][lane]
+  extern __shared__ float red[];  // per-wave partial results, [wave][tile][r][lane]
 
   const int W = (int)(blockDim.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int nl = lane & 15;  // weight row of the tile / activation row / result column
+  const int nl = lane & 15;  // weight row of a tile / activation row / result column
   const int q = lane >> 4;   // load: group of the quad; compute: chunk of the group
-  const int64_t row0 = (int64_t)blockIdx.x * 16;
-  const int rows = (int)min((int64_t)16, (int64_t)N - row0);
+  const int64_t row0 = (int64_t)blockIdx.x * (16 * TW);
+  const int rows = (int)min((int64_t)16 * TW, (int64_t)N - row0);
   const int C = 4 * G;
   const int nq = (G + 3) >> 2;
 
@@ -133,19 +134,26 @@ __global__ __launch_bounds__(1024) void linear_mfma_kernel(
   const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
   const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
 
-  float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
+  float4_t yacc[TW];
+#pragma unroll
+  for (int t = 0; t < TW; ++t) yacc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
   for (int Q = wave; Q < nq; Q += W) {
-    // 1. Loads.  Row n >= rows and x rows m >= M are past their extents.
+    // 1. Loads.  Rows past the block and x rows m >= M are past their extents.
     const int gq = 4 * Q + q;
     const bool okw = gq < G;
-    u32x4 wv[BITS];
+    u32x4 wv[TW][BITS];
+    uint32_t sraw[TW], zraw[TW];
 #pragma unroll
-    for (int p = 0; p < BITS; ++p)
-      wv[p] = __builtin_amdgcn_raw_buffer_load_b128(
-          qr, okw ? (uint32_t)(((nl * BITS + p) * C + 4 * gq) * 4) : kOffsetNone, 0, kStreamPolicyM);
-    const uint32_t sraw = __builtin_amdgcn_raw_buffer_load_b16(sr, okw ? (uint32_t)(nl * G + gq) * 2 : kOffsetNone, 0, 0);
-    const uint32_t zraw = __builtin_amdgcn_raw_buffer_load_b8(zr, okw ? (uint32_t)(nl * G + gq) : kOffsetNone, 0, 0);
+    for (int t = 0; t < TW; ++t) {
+      const int nrow = 16 * t + nl;
+#pragma unroll
+      for (int p = 0; p < BITS; ++p)
+        wv[t][p] = __builtin_amdgcn_raw_buffer_load_b128(
+            qr, okw ? (uint32_t)(((nrow * BITS + p) * C + 4 * gq) * 4) : kOffsetNone, 0, kStreamPolicyM);
+      sraw[t] = __builtin_amdgcn_raw_buffer_load_b16(sr, okw ? (uint32_t)(nrow * G + gq) * 2 : kOffsetNone, 0, 0);
+      zraw[t] = __builtin_amdgcn_raw_buffer_load_b8(zr, okw ? (uint32_t)(nrow * G + gq) : kOffsetNone, 0, 0);
+    }
     u32x4 xa[4][4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -158,50 +166,60 @@ __global__ __launch_bounds__(1024) void linear_mfma_kernel(
 
     // 2. Quarter transposes: plane words (chunk q of group 4Q + j now in
     //    component j) and the four groups' scale | zero << 16 in every quarter.
-    uint32_t wt[BITS][4];
+    uint32_t wt[TW][BITS][4];
+    uint32_t szj[TW][4];
 #pragma unroll
-    for (int p = 0; p < BITS; ++p) {
-      wt[p][0] = wv[p][0];
-      wt[p][1] = wv[p][1];
-      wt[p][2] = wv[p][2];
-      wt[p][3] = wv[p][3];
-      transpose_quarters(wt[p][0], wt[p][1], wt[p][2], wt[p][3]);
+    for (int t = 0; t < TW; ++t) {
+#pragma unroll
+      for (int p = 0; p < BITS; ++p) {
+        wt[t][p][0] = wv[t][p][0];
+        wt[t][p][1] = wv[t][p][1];
+        wt[t][p][2] = wv[t][p][2];
+        wt[t][p][3] = wv[t][p][3];
+        transpose_quarters(wt[t][p][0], wt[t][p][1], wt[t][p][2], wt[t][p][3]);
+      }
+      const uint32_t sz = sraw[t] | (zraw[t] << 16);
+      szj[t][0] = szj[t][1] = szj[t][2] = szj[t][3] = sz;
+      transpose_quarters(szj[t][0], szj[t][1], szj[t][2], szj[t][3]);
     }
-    const uint32_t sz = sraw | (zraw << 16);
-    uint32_t szj[4] = {sz, sz, sz, sz};
-    transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
 
-    // 3. Per group: exact (q - z) pairs, four MFMAs, scale.
+    // 3. Per group and tile: exact (q - z) pairs, four MFMAs, scale.
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      uint32_t w[BITS];
 #pragma unroll
-      for (int p = 0; p < BITS; ++p) w[p] = wt[p][j];
-      uint32_t pr[16];
-      unpack_chunk_exact<BITS>(w, szj[j] >> 16, pr);
-      float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < TW; ++t) {
+        uint32_t w[BITS];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const half8_t a = __builtin_bit_cast(half8_t, xa[j][jj]);
-        const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+        for (int p = 0; p < BITS; ++p) w[p] = wt[t][p][j];
+        uint32_t pr[16];
+        unpack_chunk_exact<BITS>(w, szj[t][j] >> 16, pr);
+        float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const half8_t a = __builtin_bit_cast(half8_t, xa[j][jj]);
+          const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
+          c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+        }
+        const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[t][j] & 0xFFFFu));
+        yacc[t] += s * c;
       }
-      const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[j] & 0xFFFFu));
-      yacc += s * c;
     }
   }
 
   // 4. Fixed-order reduction of the W waves' partials.
 #pragma unroll
-  for (int r = 0; r < 4; ++r) red[(wave * 4 + r) * 64 + lane] = yacc[r];
+  for (int t = 0; t < TW; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[((wave * TW + t) * 4 + r) * 64 + lane] = yacc[t][r];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < 4 * 64; idx += blockDim.x) {
-    const int r = idx >> 6;
+  for (int idx = threadIdx.x; idx < TW * 4 * 64; idx += blockDim.x) {
+    const int t = idx >> 8;
+    const int r = (idx >> 6) & 3;
     const int ln = idx & 63;
     float v = 0.0f;
-    for (int w = 0; w < W; ++w) v += red[(w * 4 + r) * 64 + ln];
+    for (int w = 0; w < W; ++w) v += red[((w * TW + t) * 4 + r) * 64 + ln];
     const int m = 4 * (ln >> 4) + r;
-    const int n = ln & 15;
+    const int n = 16 * t + (ln & 15);
     if (m < M && n < rows) y[(int64_t)m * N + row0 + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
   }
 }
@@ -215,13 +233,25 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   const int G = (int)(K / 128);
   LinearTuning& tune = linear_tuning();
   const int nq = (G + 3) / 4;
-  // One wave per quad of the row, at most 16 (longer rows loop).
-  const int W = tune.mfma_waves > 0 ? min(16, tune.mfma_waves) : min(16, nq);
-  const unsigned blocks = (unsigned)((N + 15) / 16);
+  // Two tiles per block share each activation fragment when rows are long
+  // (the fragments then outweigh the weights) and there are enough tiles to
+  // keep a block on every compute unit (measured on MI355X).
+  const int64_t tiles = (N + 15) / 16;
+  const int TW = tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1);
+  // One wave per quad of the row, at most 16 / TW (register budget; longer
+  // rows loop).
+  const int wmax = 16 / TW;
+  const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
+  const unsigned blocks = (unsigned)((tiles + TW - 1) / TW);
   tune.last_blocks = (int)blocks;
-  tune.last_rows = 16;
-  launch(linear_mfma_kernel<BITS>, dim3(blocks), dim3(64 * W), (uint32_t)W * 4 * 64 * 4, stream, ev, x, qweight,
-         scales, zeros, y, M, (int)N, G, (int)K);
+  tune.last_rows = 16 * TW;
+  const uint32_t lds = (uint32_t)W * TW * 4 * 64 * 4;
+  if (TW == 2)
+    launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
+           (int)N, G, (int)K);
+  else
+    launch(linear_mfma_kernel<BITS, 1>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
+           (int)N, G, (int)K);
   return hipGetLastError();
 }
 
