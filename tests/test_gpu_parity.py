@@ -364,3 +364,18 @@ def test_max_k(bits):
         y = gpu_linear(x, qw, s, z, bits)
         r = linear_check(y, oracle.linear(x, codes, s, z))
         assert r["ok"], (M, r)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_matrix_core_two_tiles_ragged(bits):
+    """Enough 16-row tiles and long enough rows for blocks of two tiles,
+    with a last block holding a partial tile (N = 4100 = 128 * 32 + 4)."""
+    N, K = 4100, 4096
+    say("mfma two tiles", bits, N, K)
+    w = inputs.weights(N, K, cfg=16, layer=bits)
+    codes, qw, s, z = oracle_packed(w, bits)
+    for M in (3, 8, 16):
+        x = inputs.activations(M, K, cfg=16, layer=M)
+        y = gpu_linear(x, qw, s, z, bits)
+        r = linear_check(y, oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
