@@ -35,9 +35,7 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
 // Launch-shape parameters of the GEMV (defaults tuned on MI355X; exposed
 // internally so measurement harnesses can sweep them).
 struct LinearTuning {
-  int max_blocks = 1 << 20;  // flat kernel: fewest units per thread whose grid stays within this
-  int units_per_thread = 0;  // flat kernel: 1, 2 or 4; 0 = chosen from max_blocks
-  int flat_threads = 0;      // flat kernel: threads per block (256, 512 or 1024); 0 = chosen from K
+  int flat_threads = 0;      // flat kernel: threads per block (64 .. 1024); 0 = chosen from the shape
   int last_blocks = 0;       // launch shape of the most recent flat launch (for harnesses)
   int last_rows = 0;
   int mfma_min_m = 3;        // activation rows from which the matrix-core path may be used

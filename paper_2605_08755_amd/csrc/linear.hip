@@ -429,53 +429,45 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
   {
     // Flat-unit kernel when the activation tile and the partials fit in LDS.
-    // Rows per block R fill the block's unit slots (NT threads x UPT units):
-    // few loads per lane keeps the memory pipeline flowing, and whole rows
-    // per block keep the reduction inside the block.
+    // One (row, group) unit per thread (fewest loads per lane measured best on
+    // every shape) and whole rows per block, so the reduction stays inside
+    // the block.
     LinearTuning& tune = linear_tuning();
     // Threads per block: every block stages the whole activation row, so
-    // longer rows want more rows per block (about 8 or more) to amortize it.
-    const int NT = tune.flat_threads > 0 ? tune.flat_threads : (G <= 32 ? 256 : (G <= 64 ? 512 : 1024));
+    // longer rows want more rows per block (about 8 or more) to amortize it;
+    // short rows with few of them use smaller blocks so that the grid still
+    // covers the compute units.
+    int NT = tune.flat_threads > 0 ? tune.flat_threads : (G <= 32 ? 256 : (G <= 64 ? 512 : 1024));
+    if (tune.flat_threads == 0 && MT == 1)
+      while (NT > 64 && G <= 16 && NT / 2 >= G && (N + NT / G - 1) / (NT / G) < 256) NT /= 2;
     const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
-    int upt = tune.units_per_thread;
-    if (upt == 0) {
-      upt = 4;
-      for (int u : {1, 2, 4}) {
-        const int64_t rr = max(1, NT * u / G);
-        if ((N + rr - 1) / rr <= tune.max_blocks) { upt = u; break; }
-      }
-    }
-    int R = max(1, NT * upt / G);
+    int R = max(1, NT / G);
     R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
     const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
     if (MT <= 4 && lds <= 64 * 1024) {
       const unsigned blocks = (unsigned)((N + R - 1) / R);
       tune.last_blocks = (int)blocks;
       tune.last_rows = R;
-#define LAQ_FLAT_NT(MTV, UPTV, XBV, NTV)                                                                    \
-  launch(linear_flat_kernel<BITS, MTV, NTV, UPTV, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
+#define LAQ_FLAT_NT(MTV, XBV, NTV)                                                                          \
+  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
          qweight, scales, zeros, y, M, (int)N, G, R)
-#define LAQ_FLAT(MTV, UPTV, XBV)                                  \
-  do {                                                            \
-    if (NT == 1024) LAQ_FLAT_NT(MTV, UPTV, XBV, 1024);            \
-    else if (NT == 512) LAQ_FLAT_NT(MTV, UPTV, XBV, 512);         \
-    else LAQ_FLAT_NT(MTV, UPTV, XBV, 256);                        \
+#define LAQ_FLAT(MTV, XBV)                              \
+  do {                                                  \
+    if (NT == 1024) LAQ_FLAT_NT(MTV, XBV, 1024);        \
+    else if (NT == 512) LAQ_FLAT_NT(MTV, XBV, 512);     \
+    else if constexpr (MTV > 1) LAQ_FLAT_NT(MTV, XBV, 256); \
+    else if (NT == 256) LAQ_FLAT_NT(MTV, XBV, 256);     \
+    else if (NT == 128) LAQ_FLAT_NT(MTV, XBV, 128);     \
+    else LAQ_FLAT_NT(MTV, XBV, 64);                     \
   } while (0)
-#define LAQ_FLAT_XB(MTV, UPTV)                 \
-  if (XB == 2) LAQ_FLAT(MTV, UPTV, 2);         \
-  else LAQ_FLAT(MTV, UPTV, 5);
-#define LAQ_FLAT_UPT(MTV)                      \
-  switch (upt) {                               \
-    case 1: LAQ_FLAT_XB(MTV, 1) break;         \
-    case 2: LAQ_FLAT_XB(MTV, 2) break;         \
-    default: LAQ_FLAT_XB(MTV, 4) break;        \
-  }
+#define LAQ_FLAT_XB(MTV)          \
+  if (XB == 2) LAQ_FLAT(MTV, 2);  \
+  else LAQ_FLAT(MTV, 5);
       switch (MT) {
-        case 1: LAQ_FLAT_UPT(1); break;
-        case 2: LAQ_FLAT_UPT(2); break;
-        default: LAQ_FLAT_UPT(4); break;
+        case 1: LAQ_FLAT_XB(1); break;
+        case 2: LAQ_FLAT_XB(2); break;
+        default: LAQ_FLAT_XB(4); break;
       }
-#undef LAQ_FLAT_UPT
 #undef LAQ_FLAT_XB
 #undef LAQ_FLAT
 #undef LAQ_FLAT_NT
