@@ -142,15 +142,36 @@ class Stack:
             laq.linear(self.x[(layer, self.slot_of[i])][:M], q, s, z, bits, out=self.y[i][:M])
 
 
-def time_graph(stack, M, bits, steps, warmup):
+def grouped_step(stack, M, bits):
+    """One decode step of an unfused stack with the calls that share a stage
+    issued as one grouped launch each: q,k,v | o | gate,up | down."""
+    from paper_2605_08755_amd import laq
+    idx = {}
+    for i, (layer, name, N, K) in enumerate(stack.shapes):
+        idx[(layer, name)] = i
+    for layer in range(stack.layers):
+        for members in (("q", "k", "v"), ("o",), ("gate", "up"), ("down",)):
+            ii = [idx[(layer, n)] for n in members]
+            calls = [(stack.x[(layer, stack.slot_of[i])][:M],) + tuple(stack.q[bits][i]) for i in ii]
+            outs = [stack.y[i][:M] for i in ii]
+            if len(ii) == 1:
+                laq.linear(*calls[0], bits, out=outs[0])
+            else:
+                laq.linear_group(calls, bits, outs=outs)
+
+
+def time_graph(stack, M, bits, steps, warmup, step_fn=None):
     """Capture one step into a HIP graph; time `steps` replays."""
     import torch
+    if step_fn is None:
+        def step_fn():
+            stack.step(M, bits)
     stream = torch.cuda.Stream()
     g = torch.cuda.CUDAGraph()
-    stack.step(M, bits)  # eager warm-up (loads code objects)
+    step_fn()  # eager warm-up (loads code objects)
     torch.cuda.synchronize()
     with torch.cuda.graph(g, stream=stream):
-        stack.step(M, bits)
+        step_fn()
     for _ in range(warmup):
         g.replay()
     torch.cuda.synchronize()
@@ -366,6 +387,11 @@ def main():
         unfused = {"us_per_step": round(ums * 1e3, 2), "launches_per_step": len(ustack.shapes),
                    "GBps": round(wbytes / (ums * 1e-3) / 1e9, 1)}
         log("unfused (one call per projection):", unfused)
+        gms, _ = time_graph(ustack, 1, 3, max(20, args.steps // 4), 5,
+                            step_fn=lambda: grouped_step(ustack, 1, 3))
+        unfused["grouped_launch"] = {"us_per_step": round(gms * 1e3, 2), "launches_per_step": 4 * ustack.layers,
+                                     "GBps": round(wbytes / (gms * 1e-3) / 1e9, 1)}
+        log("separate weights, shared-stage calls as grouped launches:", unfused["grouped_launch"])
         del ustack
         torch.cuda.empty_cache()
 

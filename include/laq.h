@@ -84,6 +84,7 @@ typedef int32_t laq_status;
 #define LAQ_ABI_VERSION 1
 #define LAQ_GROUP 128
 #define LAQ_MAX_M 16
+#define LAQ_MAX_GROUP 8
 
 /* ABI version of the loaded library (LAQ_ABI_VERSION it was built with). */
 int32_t laq_abi_version(void);
@@ -163,6 +164,40 @@ laq_status laq_linear_w3g128(const void *x, const uint32_t *qweight,
                              void *y, int64_t M, int64_t N, int64_t K,
                              void *stream);
 
+/*
+ * laq_linear_group_w3g128 -- several independent laq_linear_w3g128 calls
+ * (1 <= count <= LAQ_MAX_GROUP) with the same M, issued as one kernel launch:
+ * for instance the q, k and v projections of a decoder layer, which read the
+ * same activations, without concatenating their weights.  A decode step's
+ * stages depend on each other through attention and normalization, so only
+ * calls that share a stage can be grouped; one launch instead of one per
+ * call is what the grouping saves (a dependent launch costs about 1.6 us on
+ * MI355X).
+ *
+ *   calls  [in]  host array of `count` descriptors; each is validated as the
+ *                corresponding laq_linear_w3g128 call would be.  The calls
+ *                must be independent: no call's y may overlap any call's x,
+ *                weights or y.
+ *   M      [in]  activation rows of every call, 1..16.
+ *
+ * Results: each y equals that call's laq_linear_w3g128 result within the
+ * linear tolerance; on the one-row VALU path (M <= 2, and M <= 4 with rows of
+ * at most 3072) bit for bit.  One activation row longer than the LDS holds
+ * (K > ~29000) makes the group one launch per call, with the same results.
+ */
+typedef struct laq_linear_call {
+    const void *x;            /* fp16 [M][K] */
+    const uint32_t *qweight;  /* [N][bits][K/32] */
+    const void *scales;       /* fp16 [N][K/128] */
+    const uint8_t *zeros;     /* uint8 [N][K/128] */
+    void *y;                  /* fp16 [M][N] (output) */
+    int64_t N;
+    int64_t K;
+} laq_linear_call;
+
+laq_status laq_linear_group_w3g128(const laq_linear_call *calls, int32_t count, int64_t M,
+                                   void *stream);
+
 /* W4G128 siblings: same contracts with 4-bit codes (0..15), s = (hi-lo)/15,
  * zero points 0..15, qweight uint32 [N][4][K/32] (N*K/2 bytes). */
 laq_status laq_quantize_w4g128(const void *w, int64_t N, int64_t K,
@@ -171,6 +206,9 @@ laq_status laq_quantize_w4g128(const void *w, int64_t N, int64_t K,
 
 laq_status laq_pack_w4g128(const void *w, const void *scales, const uint8_t *zeros,
                            int64_t N, int64_t K, uint32_t *qweight, void *stream);
+
+laq_status laq_linear_group_w4g128(const laq_linear_call *calls, int32_t count, int64_t M,
+                                   void *stream);
 
 laq_status laq_linear_w4g128(const void *x, const uint32_t *qweight,
                              const void *scales, const uint8_t *zeros,

@@ -91,6 +91,29 @@ laq_status linear(const char* fn, const void* x, const uint32_t* qweight, const 
                                                  static_cast<hipStream_t>(stream), ev));
 }
 
+template <int BITS>
+laq_status linear_group(const char* fn, const laq_linear_call* calls, int32_t count, int64_t M, void* stream) {
+  const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
+  if (!calls) return fail(LAQ_ERR_NULL_POINTER, fn, "null calls array");
+  if (count < 1 || count > LAQ_MAX_GROUP) return fail(LAQ_ERR_BAD_SHAPE, fn, "count must be in 1..8");
+  if (M < 1 || M > LAQ_MAX_M) return fail(LAQ_ERR_BAD_M, fn, "M must be in 1..16");
+  laq::LinearCall lc[laq::kMaxGroup];
+  int64_t blocks = 0;
+  for (int i = 0; i < count; ++i) {
+    const laq_linear_call& c = calls[i];
+    if (!c.x || !c.qweight || !c.scales || !c.zeros || !c.y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer in a call");
+    laq_status st = check_shape(fn, c.N, c.K);
+    if (st != LAQ_OK) return st;
+    if (!aligned(c.x, 16) || !aligned(c.qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "x and qweight must be 16-byte aligned");
+    if (!aligned(c.scales, 2) || !aligned(c.y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+    blocks += c.N;  // an upper bound of the grid: at least one row per block
+    lc[i] = laq::LinearCall{static_cast<const uint16_t*>(c.x), c.qweight, static_cast<const uint16_t*>(c.scales),
+                            c.zeros, static_cast<uint16_t*>(c.y), (int)c.N, (int)(c.K / 128), 0, 0};
+  }
+  if (blocks >= (1LL << 31)) return fail(LAQ_ERR_BAD_SHAPE, fn, "the calls' rows must total < 2^31");
+  return hip_status(fn, laq::launch_linear_group<BITS>(lc, count, (int)M, static_cast<hipStream_t>(stream), ev));
+}
+
 }  // namespace
 
 extern "C" {
@@ -141,6 +164,14 @@ laq_status laq_linear_w3g128(const void* x, const uint32_t* qweight, const void*
                              const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
                              void* stream) {
   return linear<3>("laq_linear_w3g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+laq_status laq_linear_group_w3g128(const laq_linear_call* calls, int32_t count, int64_t M, void* stream) {
+  return linear_group<3>("laq_linear_group_w3g128", calls, count, M, stream);
+}
+
+laq_status laq_linear_group_w4g128(const laq_linear_call* calls, int32_t count, int64_t M, void* stream) {
+  return linear_group<4>("laq_linear_group_w4g128", calls, count, M, stream);
 }
 
 laq_status laq_linear_w4g128(const void* x, const uint32_t* qweight, const void* scales,

@@ -44,6 +44,23 @@ struct LinearTuning {
 };
 LinearTuning& linear_tuning();
 
+// Several independent linears in one launch (kernel argument block, by value).
+constexpr int kMaxGroup = 8;
+struct LinearCall {
+  const uint16_t* x;
+  const uint32_t* qw;
+  const uint16_t* scales;
+  const uint8_t* zeros;
+  uint16_t* y;
+  int N, G;
+  int R;            // rows per block (flat kernel) or 16-row tiles per block (matrix cores: 1)
+  int first_block;  // first block of this call in the grid
+};
+struct LinearGroup {
+  LinearCall call[kMaxGroup];
+  int count;
+};
+
 // Launchers (return the HIP error of the launch; shapes already validated).
 template <int BITS>
 hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qweight,
@@ -58,6 +75,14 @@ template <int BITS>
 hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                               const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
                               hipStream_t stream, const LaunchEvents& ev);
+
+// calls[i].{x, qw, scales, zeros, y, N, G} filled in by the caller; count in 1..kMaxGroup.
+template <int BITS>
+hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t stream, const LaunchEvents& ev);
+
+template <int BITS>
+hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStream_t stream,
+                                    const LaunchEvents& ev);
 
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,

@@ -21,6 +21,8 @@
 // exact power of two once per group, and the zero point enters once per
 // group as z * sum_k x[m][k] (the per-group activation sums are computed
 // while staging x).
+#include <algorithm>
+
 #include "laq_internal.h"
 
 namespace laq {
@@ -264,17 +266,18 @@ __device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[XB], int base, in
   }
 }
 
+// One block of the flat kernel: rows block*R .. block*R + R - 1 of one call.
 template <int BITS, int MT, int NT, int UPT, int XB>
-__global__ __launch_bounds__(NT) void linear_flat_kernel(
+__device__ __forceinline__ void flat_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R) {
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, int block) {
   extern __shared__ u32x4 lds[];
   u32x4* xl = lds;                                                                // [MT][G][17]
   float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
   float* part = xsum + MT * G;                                                    // [MT][R*G]
 
   const int t = threadIdx.x;
-  const int64_t row0 = (int64_t)blockIdx.x * R;
+  const int64_t row0 = (int64_t)block * R;
   const int rows = (int)min((int64_t)R, (int64_t)N - row0);
   const int U = rows * G;
   const int XU = MT * G * 16;  // activation tile in 16-byte units (rows m >= M read as zero)
@@ -401,6 +404,27 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
   }
 }
 
+template <int BITS, int MT, int NT, int UPT, int XB>
+__global__ __launch_bounds__(NT) void linear_flat_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R) {
+  flat_block<BITS, MT, NT, UPT, XB>(x, qw, scales, zeros, y, M, N, G, R, (int)blockIdx.x);
+}
+
+// Several independent calls in one launch: block b belongs to the last call
+// whose first block is <= b.  The call's fields are picked with constant
+// indices (uniform selects), so the argument block is never indexed at run
+// time.
+template <int BITS, int MT, int NT, int UPT, int XB>
+__global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup grp, int M) {
+  const int b = (int)blockIdx.x;
+  LinearCall c = grp.call[0];
+#pragma unroll
+  for (int j = 1; j < kMaxGroup; ++j)
+    if (j < grp.count && b >= grp.call[j].first_block) c = grp.call[j];
+  flat_block<BITS, MT, NT, UPT, XB>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, c.R, b - c.first_block);
+}
+
 int ceil_pow2(int v) {
   int p = 1;
   while (p < v) p <<= 1;
@@ -505,6 +529,67 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   return hipGetLastError();
 }
 
+template <int BITS>
+hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t stream, const LaunchEvents& ev) {
+  int G_max = 1;
+  for (int i = 0; i < count; ++i) G_max = max(G_max, calls[i].G);
+  const int MT = ceil_pow2(M);
+  // Same routing as a single call, decided on the longest row of the group.
+  if (M >= linear_tuning().mfma_min_m && !(M <= 4 && G_max <= 24))
+    return launch_linear_mfma_group<BITS>(calls, count, M, stream, ev);
+  const int NT = G_max <= 32 ? 256 : (G_max <= 64 ? 512 : 1024);
+  const int XB = (MT * G_max * 16 <= 2 * NT) ? 2 : 5;
+  size_t lds = 0;
+  int64_t blocks = 0;
+  LinearGroup grp{};
+  for (int i = 0; i < count; ++i) {
+    LinearCall& c = calls[i];
+    c.R = max(1, min(max(1, NT / c.G), 4096 / (c.G * MT)));
+    lds = std::max(lds, (size_t)MT * c.G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * c.R * c.G * 4);
+    c.first_block = (int)blocks;
+    blocks += (c.N + c.R - 1) / c.R;
+    grp.call[i] = c;
+  }
+  grp.count = count;
+  if (MT > 4 || lds > 64 * 1024) {
+    if (M >= 2) return launch_linear_mfma_group<BITS>(calls, count, M, stream, ev);
+    // One activation row too long for LDS: one launch per call.
+    for (int i = 0; i < count; ++i) {
+      const LinearCall& c = calls[i];
+      LaunchEvents e_i;  // the measurement hook spans the whole sequence
+      e_i.start = i == 0 ? ev.start : nullptr;
+      e_i.stop = i == count - 1 ? ev.stop : nullptr;
+      const hipError_t e = launch_linear<BITS>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, (int64_t)c.G * 128,
+                                               stream, e_i);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+#define LAQ_FLAT_G(MTV, XBV, NTV)                                                                         \
+  launch(linear_flat_group_kernel<BITS, MTV, NTV, 1, XBV>, dim3((unsigned)blocks), dim3(NTV), (uint32_t)lds, \
+         stream, ev, grp, M)
+#define LAQ_FLAT_GN(MTV, XBV)                              \
+  do {                                                     \
+    if (NT == 1024) LAQ_FLAT_G(MTV, XBV, 1024);            \
+    else if (NT == 512) LAQ_FLAT_G(MTV, XBV, 512);         \
+    else LAQ_FLAT_G(MTV, XBV, 256);                        \
+  } while (0)
+#define LAQ_FLAT_GX(MTV)           \
+  if (XB == 2) LAQ_FLAT_GN(MTV, 2); \
+  else LAQ_FLAT_GN(MTV, 5);
+  switch (MT) {
+    case 1: LAQ_FLAT_GX(1); break;
+    case 2: LAQ_FLAT_GX(2); break;
+    default: LAQ_FLAT_GX(4); break;
+  }
+#undef LAQ_FLAT_GX
+#undef LAQ_FLAT_GN
+#undef LAQ_FLAT_G
+  return hipGetLastError();
+}
+
+template hipError_t launch_linear_group<3>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
+template hipError_t launch_linear_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
                                      uint16_t*, int, int64_t, int64_t, hipStream_t,
                                      const LaunchEvents&);

@@ -114,17 +114,18 @@ __device__ __forceinline__ void transpose_quarters(uint32_t& r0, uint32_t& r1, u
 // the quad, the layout the matrix core wants (lane (n, q) supplies row n's
 // codes 32q .. 32q+31 of the group).  Slots past the last group read zeros.
 template <int BITS, int TW>
-__global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
+__device__ __forceinline__ void mfma_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int K) {
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
   extern __shared__ float red[];  // per-wave partial results, [wave][tile][r][lane]
 
+  const int K = 128 * G;
   const int W = (int)(blockDim.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nl = lane & 15;  // weight row of a tile / activation row / result column
   const int q = lane >> 4;   // load: group of the quad; compute: chunk of the group
-  const int64_t row0 = (int64_t)blockIdx.x * (16 * TW);
+  const int64_t row0 = (int64_t)block * (16 * TW);
   const int rows = (int)min((int64_t)16 * TW, (int64_t)N - row0);
   const int C = 4 * G;
   const int nq = (G + 3) >> 2;
@@ -224,6 +225,25 @@ __global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
   }
 }
 
+template <int BITS, int TW>
+__global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G) {
+  mfma_block<BITS, TW>(x, qw, scales, zeros, y, M, N, G, (int)blockIdx.x);
+}
+
+// Several independent calls in one launch (one 16-row tile per block); the
+// call of block b is picked with constant indices, as in the flat kernel.
+template <int BITS>
+__global__ __launch_bounds__(1024) void linear_mfma_group_kernel(const LinearGroup grp, int M) {
+  const int b = (int)blockIdx.x;
+  LinearCall c = grp.call[0];
+#pragma unroll
+  for (int j = 1; j < kMaxGroup; ++j)
+    if (j < grp.count && b >= grp.call[j].first_block) c = grp.call[j];
+  mfma_block<BITS, 1>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, b - c.first_block);
+}
+
 }  // namespace
 
 template <int BITS>
@@ -248,13 +268,36 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   const uint32_t lds = (uint32_t)W * TW * 4 * 64 * 4;
   if (TW == 2)
     launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
-           (int)N, G, (int)K);
+           (int)N, G);
   else
     launch(linear_mfma_kernel<BITS, 1>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
-           (int)N, G, (int)K);
+           (int)N, G);
   return hipGetLastError();
 }
 
+template <int BITS>
+hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStream_t stream,
+                                    const LaunchEvents& ev) {
+  int nq_max = 1;
+  int64_t blocks = 0;
+  LinearGroup grp{};
+  for (int i = 0; i < count; ++i) {
+    LinearCall& c = calls[i];
+    nq_max = max(nq_max, (c.G + 3) / 4);
+    c.R = 1;
+    c.first_block = (int)blocks;
+    blocks += (c.N + 15) / 16;
+    grp.call[i] = c;
+  }
+  grp.count = count;
+  const int W = min(16, nq_max);
+  launch(linear_mfma_group_kernel<BITS>, dim3((unsigned)blocks), dim3(64 * W), (uint32_t)W * 4 * 64 * 4, stream, ev,
+         grp, M);
+  return hipGetLastError();
+}
+
+template hipError_t launch_linear_mfma_group<3>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
+template hipError_t launch_linear_mfma_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_mfma<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
                                           uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_mfma<4>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,

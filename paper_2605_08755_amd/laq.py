@@ -20,9 +20,17 @@ LAQ_ERR_HIP = 5
 MAX_M = 16
 GROUP = 128
 
+MAX_GROUP = 8
+
 EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profile_next_launch",
-           "laq_quantize_w3g128", "laq_pack_w3g128", "laq_linear_w3g128",
-           "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128")
+           "laq_quantize_w3g128", "laq_pack_w3g128", "laq_linear_w3g128", "laq_linear_group_w3g128",
+           "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128", "laq_linear_group_w4g128")
+
+
+class LinearCall(ctypes.Structure):
+    """laq_linear_call of include/laq.h."""
+    _fields_ = [("x", ctypes.c_void_p), ("qweight", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("zeros", ctypes.c_void_p), ("y", ctypes.c_void_p), ("N", ctypes.c_int64), ("K", ctypes.c_int64)]
 
 _lib = None
 
@@ -57,6 +65,10 @@ def lib():
         for name in ("laq_pack_w3g128", "laq_pack_w4g128"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, I64, I64, P, P]
+            f.restype = ctypes.c_int32
+        for name in ("laq_linear_group_w3g128", "laq_linear_group_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [ctypes.POINTER(LinearCall), ctypes.c_int32, I64, P]
             f.restype = ctypes.c_int32
         for name in ("laq_linear_w3g128", "laq_linear_w4g128"):
             f = getattr(L, name)
@@ -141,6 +153,34 @@ def linear(x, qweight, scales, zeros, bits=3, out=None):
     fn = lib().laq_linear_w3g128 if bits == 3 else lib().laq_linear_w4g128
     _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _stream(x.device)))
     return y
+
+
+def linear_group(calls, bits=3, outs=None):
+    """Several independent linears with the same M in one launch.
+
+    calls: sequence of (x, qweight, scales, zeros) as for `linear`; returns
+    the list of y (or fills `outs`)."""
+    import torch
+    n = len(calls)
+    assert 1 <= n <= MAX_GROUP
+    arr = (LinearCall * n)()
+    ys = []
+    M = None
+    for i, (x, qweight, scales, zeros) in enumerate(calls):
+        assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+        Mi, K = x.shape
+        M = Mi if M is None else M
+        assert Mi == M, "every call of a group has the same M"
+        N = scales.shape[0]
+        assert qweight.numel() == packed_words(bits, N, K) and qweight.is_contiguous()
+        assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+        assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device) if outs is None else outs[i]
+        ys.append(y)
+        arr[i] = LinearCall(x.data_ptr(), qweight.data_ptr(), scales.data_ptr(), zeros.data_ptr(), y.data_ptr(), N, K)
+    fn = lib().laq_linear_group_w3g128 if bits == 3 else lib().laq_linear_group_w4g128
+    _check(fn(arr, n, M, _stream(calls[0][0].device)))
+    return ys
 
 
 def quantize_w3g128(w, out=None):

@@ -107,6 +107,33 @@ def test_linear_validation(L, bits):
     assert b"laq_linear" in L.laq_last_error()
 
 
+@pytest.mark.parametrize("bits", [3, 4])
+def test_group_validation(L, bits):
+    f = L.laq_linear_group_w3g128 if bits == 3 else L.laq_linear_group_w4g128
+
+    def calls(n, **kw):
+        arr = (laq.LinearCall * max(n, 1))()
+        for i in range(n):
+            d = dict(x=FAKE, qweight=FAKE, scales=FAKE, zeros=FAKE, y=FAKE, N=4, K=128)
+            if i == n - 1:
+                d.update(kw)
+            arr[i] = laq.LinearCall(d["x"], d["qweight"], d["scales"], d["zeros"], d["y"], d["N"], d["K"])
+        return arr
+
+    assert f(None, 1, 1, None) == laq.LAQ_ERR_NULL_POINTER
+    assert f(calls(1), 0, 1, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(calls(9), 9, 1, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(calls(2), 2, 0, None) == laq.LAQ_ERR_BAD_M
+    assert f(calls(2), 2, 17, None) == laq.LAQ_ERR_BAD_M
+    for kw in ("x", "qweight", "scales", "zeros", "y"):
+        assert f(calls(3, **{kw: 0}), 3, 1, None) == laq.LAQ_ERR_NULL_POINTER
+    assert f(calls(2, K=100), 2, 1, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(calls(2, N=0), 2, 1, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(calls(2, x=FAKE + 2), 2, 1, None) == laq.LAQ_ERR_MISALIGNED
+    assert f(calls(2, y=FAKE + 1), 2, 1, None) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_linear_group" in L.laq_last_error()
+
+
 def test_shape_check_precedes_m_check(L):
     # a bad shape is reported even when M is also bad
     assert _lin(L, 3, M=0, K=100) == laq.LAQ_ERR_BAD_SHAPE

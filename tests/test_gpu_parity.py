@@ -379,3 +379,63 @@ def test_matrix_core_two_tiles_ragged(bits):
         y = gpu_linear(x, qw, s, z, bits)
         r = linear_check(y, oracle.linear(x, codes, s, z))
         assert r["ok"], (M, r)
+
+
+# ---------------------------------------------------------------------------
+# grouped calls: several independent linears in one launch
+# ---------------------------------------------------------------------------
+def _group_case(bits, specs, M, cfg):
+    """specs: list of (N, K, x_slot); calls sharing a slot share x."""
+    xs = {}
+    calls, refs = [], []
+    for i, (N, K, slot) in enumerate(specs):
+        if slot not in xs:
+            xs[slot] = inputs.activations(M, K, cfg=cfg, layer=slot)
+        x = xs[slot]
+        w = inputs.weights(N, K, cfg=cfg, layer=i, proj=bits)
+        codes, qw, s, z = oracle_packed(w, bits)
+        calls.append((to_dev(x), to_dev(qw.view(np.int32)), to_dev(s.view(np.float16)), to_dev(z)))
+        refs.append(oracle.linear(x, codes, s, z))
+    ys = laq.linear_group(calls, bits)
+    singles = [laq.linear(*c, bits) for c in calls]
+    torch.cuda.synchronize()
+    return [y.cpu().numpy() for y in ys], [y.cpu().numpy() for y in singles], refs
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 8, 16])
+def test_group_qkv(bits, M):
+    """q, k, v of a Qwen3-4B layer (same activations) as one launch."""
+    say("group qkv", bits, M)
+    ys, singles, refs = _group_case(bits, [(4096, 2560, 0), (1024, 2560, 0), (1024, 2560, 0)], M, cfg=40)
+    for y, y1, ref in zip(ys, singles, refs):
+        r = linear_check(y, ref)
+        assert r["ok"], r
+        if M <= 4:  # one-row VALU path: the same kernel body, bit for bit
+            assert np.array_equal(y.view(np.uint16), y1.view(np.uint16))
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("M", [1, 2, 16])
+def test_group_mixed(bits, M):
+    """Eight calls of different shapes (the most a group takes): several K,
+    ragged N, a single row, separate activations."""
+    say("group mixed", bits, M)
+    specs = [(2560, 4096, 0), (257, 9728, 1), (1, 128, 2), (300, 2560, 3), (17, 384, 4),
+             (1024, 1024, 5), (96, 9728, 1), (64, 128, 6)]
+    ys, singles, refs = _group_case(bits, specs, M, cfg=41)
+    for y, y1, ref in zip(ys, singles, refs):
+        r = linear_check(y, ref)
+        assert r["ok"], r
+        if M <= 2:
+            assert np.array_equal(y.view(np.uint16), y1.view(np.uint16))
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_group_long_rows_one_row(bits):
+    """M = 1 with a row longer than LDS holds: one launch per call, same results."""
+    say("group long rows", bits)
+    ys, singles, refs = _group_case(bits, [(5, 32768, 0), (3, 32768, 0)], 1, cfg=42)
+    for y, y1, ref in zip(ys, singles, refs):
+        assert linear_check(y, ref)["ok"]
+        assert np.array_equal(y.view(np.uint16), y1.view(np.uint16))
