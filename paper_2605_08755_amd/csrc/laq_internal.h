@@ -16,6 +16,21 @@ typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ half2_t as_half2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
 
+// XCD-aware block order.  MI355X deals consecutive workgroups of a launch to
+// its eight XCDs in turn, and each XCD has its own L2.  A grid of
+// xcd_grid(nblocks) workgroups (a multiple of 8) whose workgroup b takes
+// logical block xcd_block() = (b % 8) * (grid / 8) + b / 8 gives every XCD a
+// contiguous range of logical blocks (rows); logical blocks >= nblocks are
+// idle and return at once.  Any mapping of workgroups to XCDs gives the same
+// results: this is a permutation of independent blocks.
+inline unsigned xcd_grid(int64_t nblocks) { return (unsigned)(((nblocks + 7) / 8) * 8); }
+
+__device__ __forceinline__ int xcd_block() {
+  const int per = (int)(gridDim.x >> 3);
+  const int b = (int)blockIdx.x;
+  return (b & 7) * per + (b >> 3);
+}
+
 // Optional events recorded at the kernel's execution start and end
 // (hipExtLaunchKernelGGL); both null for an ordinary launch.
 struct LaunchEvents {
@@ -59,6 +74,7 @@ struct LinearCall {
 struct LinearGroup {
   LinearCall call[kMaxGroup];
   int count;
+  int blocks;  // logical blocks of all calls (the grid is rounded up to a multiple of 8)
 };
 
 // Launchers (return the HIP error of the launch; shapes already validated).

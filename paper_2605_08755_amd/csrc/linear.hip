@@ -408,7 +408,9 @@ template <int BITS, int MT, int NT, int UPT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R) {
-  flat_block<BITS, MT, NT, UPT, XB>(x, qw, scales, zeros, y, M, N, G, R, (int)blockIdx.x);
+  const int block = xcd_block();
+  if (block >= (int)(((int64_t)N + R - 1) / R)) return;  // idle slot of the XCD-rounded grid
+  flat_block<BITS, MT, NT, UPT, XB>(x, qw, scales, zeros, y, M, N, G, R, block);
 }
 
 // Several independent calls in one launch: block b belongs to the last call
@@ -417,7 +419,8 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
 // time.
 template <int BITS, int MT, int NT, int UPT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup grp, int M) {
-  const int b = (int)blockIdx.x;
+  const int b = xcd_block();
+  if (b >= grp.blocks) return;  // idle slot of the XCD-rounded grid
   LinearCall c = grp.call[0];
 #pragma unroll
   for (int j = 1; j < kMaxGroup; ++j)
@@ -469,8 +472,8 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
     const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
     if (MT <= 4 && lds <= 64 * 1024) {
-      const unsigned blocks = (unsigned)((N + R - 1) / R);
-      tune.last_blocks = (int)blocks;
+      const unsigned blocks = xcd_grid((N + R - 1) / R);
+      tune.last_blocks = (int)((N + R - 1) / R);
       tune.last_rows = R;
 #define LAQ_FLAT_NT(MTV, XBV, NTV)                                                                          \
   launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
@@ -551,6 +554,7 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
     grp.call[i] = c;
   }
   grp.count = count;
+  grp.blocks = (int)blocks;
   if (MT > 4 || lds > 64 * 1024) {
     if (M >= 2) return launch_linear_mfma_group<BITS>(calls, count, M, stream, ev);
     // One activation row too long for LDS: one launch per call.
@@ -566,7 +570,7 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
     return hipSuccess;
   }
 #define LAQ_FLAT_G(MTV, XBV, NTV)                                                                         \
-  launch(linear_flat_group_kernel<BITS, MTV, NTV, 1, XBV>, dim3((unsigned)blocks), dim3(NTV), (uint32_t)lds, \
+  launch(linear_flat_group_kernel<BITS, MTV, NTV, 1, XBV>, dim3(xcd_grid(blocks)), dim3(NTV), (uint32_t)lds, \
          stream, ev, grp, M)
 #define LAQ_FLAT_GN(MTV, XBV)                              \
   do {                                                     \

@@ -229,14 +229,17 @@ template <int BITS, int TW>
 __global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G) {
-  mfma_block<BITS, TW>(x, qw, scales, zeros, y, M, N, G, (int)blockIdx.x);
+  const int block = xcd_block();
+  if (block >= (int)(((int64_t)N + 16 * TW - 1) / (16 * TW))) return;  // idle slot of the XCD-rounded grid
+  mfma_block<BITS, TW>(x, qw, scales, zeros, y, M, N, G, block);
 }
 
 // Several independent calls in one launch (one 16-row tile per block); the
 // call of block b is picked with constant indices, as in the flat kernel.
 template <int BITS>
 __global__ __launch_bounds__(1024) void linear_mfma_group_kernel(const LinearGroup grp, int M) {
-  const int b = (int)blockIdx.x;
+  const int b = xcd_block();
+  if (b >= grp.blocks) return;  // idle slot of the XCD-rounded grid
   LinearCall c = grp.call[0];
 #pragma unroll
   for (int j = 1; j < kMaxGroup; ++j)
@@ -262,8 +265,8 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   // rows loop).
   const int wmax = 16 / TW;
   const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
-  const unsigned blocks = (unsigned)((tiles + TW - 1) / TW);
-  tune.last_blocks = (int)blocks;
+  const unsigned blocks = xcd_grid((tiles + TW - 1) / TW);
+  tune.last_blocks = (int)((tiles + TW - 1) / TW);
   tune.last_rows = 16 * TW;
   const uint32_t lds = (uint32_t)W * TW * 4 * 64 * 4;
   if (TW == 2)
@@ -290,8 +293,9 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
     grp.call[i] = c;
   }
   grp.count = count;
+  grp.blocks = (int)blocks;
   const int W = min(16, nq_max);
-  launch(linear_mfma_group_kernel<BITS>, dim3((unsigned)blocks), dim3(64 * W), (uint32_t)W * 4 * 64 * 4, stream, ev,
+  launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * 4 * 64 * 4, stream, ev,
          grp, M);
   return hipGetLastError();
 }
