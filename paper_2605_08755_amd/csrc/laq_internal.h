@@ -70,6 +70,7 @@ struct LinearCall {
   int N, G;
   int R;            // rows per block (flat kernel) or 16-row tiles per block (matrix cores: 1)
   int first_block;  // first block of this call in the grid
+  float inv_g;      // fl(1 / G) (flat kernel)
 };
 struct LinearGroup {
   LinearCall call[kMaxGroup];

@@ -270,15 +270,18 @@ __device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[XB], int base, in
 template <int BITS, int MT, int NT, int UPT, int XB>
 __device__ __forceinline__ void flat_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, int block) {
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
+    int block) {
   extern __shared__ u32x4 lds[];
   u32x4* xl = lds;                                                                // [MT][G][17]
   float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
   float* part = xsum + MT * G;                                                    // [MT][R*G]
 
   const int t = threadIdx.x;
+  // An idle block (an XCD-rounding slot past the last row) has rows = 0: every
+  // buffer extent is zero, so it loads and stores nothing.
   const int64_t row0 = (int64_t)block * R;
-  const int rows = (int)min((int64_t)R, (int64_t)N - row0);
+  const int rows = (int)max((int64_t)0, min((int64_t)R, (int64_t)N - row0));
   const int U = rows * G;
   const int XU = MT * G * 16;  // activation tile in 16-byte units (rows m >= M read as zero)
 
@@ -289,8 +292,11 @@ __device__ __forceinline__ void flat_block(
 
   // Unit t + i*NT is (row r, group g); (r, g) advance by (NT / G, NT % G)
   // per step.  Computed before any load so that no load waits on it.
+  // t / G as trunc((t + 0.5) * fl(1/G)): the quotient's fractional part is at
+  // least 0.5/G away from an integer and the float error is below 1025 * 2^-23 / G,
+  // so the truncation is exact for every t < 1024 and G >= 1.
   const int dr = NT / G, dg = NT - (NT / G) * G;
-  const int r0 = t / G;
+  const int r0 = (int)(((float)t + 0.5f) * inv_g);
   const int g0 = t - r0 * G;
   __builtin_amdgcn_sched_barrier(0);
 
@@ -407,10 +413,12 @@ __device__ __forceinline__ void flat_block(
 template <int BITS, int MT, int NT, int UPT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R) {
-  const int block = xcd_block();
-  if (block >= (int)(((int64_t)N + R - 1) / R)) return;  // idle slot of the XCD-rounded grid
-  flat_block<BITS, MT, NT, UPT, XB>(x, qw, scales, zeros, y, M, N, G, R, block);
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
+    int nblocks) {
+  // Slots of the XCD-rounded grid past nblocks get rows = 0 in flat_block (no
+  // early return: the argument loads then go out as one batch).
+  (void)nblocks;
+  flat_block<BITS, MT, NT, UPT, XB>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
 }
 
 // Several independent calls in one launch: block b belongs to the last call
@@ -419,13 +427,13 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
 // time.
 template <int BITS, int MT, int NT, int UPT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup grp, int M) {
+  // Slots past the last call's blocks fall to that call with rows = 0.
   const int b = xcd_block();
-  if (b >= grp.blocks) return;  // idle slot of the XCD-rounded grid
   LinearCall c = grp.call[0];
 #pragma unroll
   for (int j = 1; j < kMaxGroup; ++j)
     if (j < grp.count && b >= grp.call[j].first_block) c = grp.call[j];
-  flat_block<BITS, MT, NT, UPT, XB>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, c.R, b - c.first_block);
+  flat_block<BITS, MT, NT, UPT, XB>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, c.R, c.inv_g, b - c.first_block);
 }
 
 int ceil_pow2(int v) {
@@ -472,12 +480,13 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
     const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
     if (MT <= 4 && lds <= 64 * 1024) {
-      const unsigned blocks = xcd_grid((N + R - 1) / R);
-      tune.last_blocks = (int)((N + R - 1) / R);
+      const int nblocks = (int)((N + R - 1) / R);
+      const unsigned blocks = xcd_grid(nblocks);
+      tune.last_blocks = nblocks;
       tune.last_rows = R;
 #define LAQ_FLAT_NT(MTV, XBV, NTV)                                                                          \
   launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
-         qweight, scales, zeros, y, M, (int)N, G, R)
+         qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
 #define LAQ_FLAT(MTV, XBV)                              \
   do {                                                  \
     if (NT == 1024) LAQ_FLAT_NT(MTV, XBV, 1024);        \
@@ -548,6 +557,7 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
   for (int i = 0; i < count; ++i) {
     LinearCall& c = calls[i];
     c.R = max(1, min(max(1, NT / c.G), 4096 / (c.G * MT)));
+    c.inv_g = 1.0f / (float)c.G;
     lds = std::max(lds, (size_t)MT * c.G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * c.R * c.G * 4);
     c.first_block = (int)blocks;
     blocks += (c.N + c.R - 1) / c.R;

@@ -228,9 +228,9 @@ __device__ __forceinline__ void mfma_block(
 template <int BITS, int TW>
 __global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G) {
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
   const int block = xcd_block();
-  if (block >= (int)(((int64_t)N + 16 * TW - 1) / (16 * TW))) return;  // idle slot of the XCD-rounded grid
+  if (block >= nblocks) return;  // idle slot of the XCD-rounded grid
   mfma_block<BITS, TW>(x, qw, scales, zeros, y, M, N, G, block);
 }
 
@@ -265,16 +265,17 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   // rows loop).
   const int wmax = 16 / TW;
   const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
-  const unsigned blocks = xcd_grid((tiles + TW - 1) / TW);
-  tune.last_blocks = (int)((tiles + TW - 1) / TW);
+  const int nblocks = (int)((tiles + TW - 1) / TW);
+  const unsigned blocks = xcd_grid(nblocks);
+  tune.last_blocks = nblocks;
   tune.last_rows = 16 * TW;
   const uint32_t lds = (uint32_t)W * TW * 4 * 64 * 4;
   if (TW == 2)
     launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
-           (int)N, G);
+           (int)N, G, nblocks);
   else
     launch(linear_mfma_kernel<BITS, 1>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
-           (int)N, G);
+           (int)N, G, nblocks);
   return hipGetLastError();
 }
 
