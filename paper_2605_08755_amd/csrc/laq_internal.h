@@ -56,6 +56,7 @@ struct LinearTuning {
   int mfma_min_m = 3;        // activation rows from which the matrix-core path may be used
   int mfma_waves = 0;        // matrix-core kernel: waves per block (1..16); 0 = one per group quad
   int mfma_tiles = 0;        // matrix-core kernel: 16-row tiles per block (1 or 2); 0 = chosen from N
+  int mfma_share_min_tiles = 1024;  // from this many 16-row tiles: four tiles per block share the activations
 };
 LinearTuning& linear_tuning();
 

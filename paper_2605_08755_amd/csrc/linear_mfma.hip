@@ -17,6 +17,8 @@
 //
 // The waves of a block split the groups of the block's 16 rows; their
 // partial sums are added in a fixed order through LDS (deterministic).
+#include <type_traits>
+
 #include "laq_internal.h"
 
 namespace laq {
@@ -37,17 +39,29 @@ __device__ __forceinline__ uint32_t pk_add_f16(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2_t, a) + __builtin_bit_cast(half2_t, b));
 }
 
+// (a & m) | c in one v_and_or_b32.  The mask lives in a scalar register and
+// the magic constant in a vector register (a VOP3 instruction takes no
+// literal on this target, and at most one scalar operand); left to itself the
+// compiler emits a v_and_b32 and a v_or_b32 with literals instead.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t m, uint32_t c) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "s"(m), "v"(c));  // mask from a scalar register
+  return r;
+}
+
 // fp16 bit patterns of -(2^(10-p) + z) in both halves, for the field
-// offsets used by the layouts (ulp of 2^(10-p) is 2^-p, so + z is + z*2^p ulps).
-__device__ __forceinline__ uint32_t neg_magic(uint32_t base_bits, uint32_t z, uint32_t shift) {
-  const uint32_t h = base_bits + (z << shift);
-  return h | (h << 16);
+// offsets used by the layouts (ulp of 2^(10-p) is 2^-p, so + z is + z*2^p
+// ulps).  zz holds z in both 16-bit halves; z << shift < 2^11, so no carry
+// crosses between the halves.
+__device__ __forceinline__ uint32_t neg_magic(uint32_t base_bits, uint32_t zz, uint32_t shift) {
+  return (base_bits | (base_bits << 16)) + (zz << shift);
 }
 
 // Exact (q - z) pairs of one 32-code chunk, in natural order: pair t holds
 // codes 2t (low half) and 2t+1 (high half).
 template <int BITS>
-__device__ __forceinline__ void unpack_chunk_exact(const uint32_t (&w)[BITS], uint32_t z, uint32_t (&pr)[16]) {
+__device__ __forceinline__ void unpack_chunk_exact(const uint32_t (&w)[BITS], uint32_t z1, uint32_t (&pr)[16]) {
+  const uint32_t z = z1 | (z1 << 16);
   if constexpr (BITS == 3) {
     const uint32_t n0 = neg_magic(0xE400u, z, 0);  // -(1024 + z): fields at bits 0-2
     const uint32_t n3 = neg_magic(0xD800u, z, 3);  // -(128 + z):  bits 3-5
@@ -56,11 +70,11 @@ __device__ __forceinline__ void unpack_chunk_exact(const uint32_t (&w)[BITS], ui
 #pragma unroll
     for (int p = 0; p < 3; ++p) {
       const uint32_t t = w[p] >> 10;
-      pr[5 * p + 0] = pk_add_f16((w[p] & 0x00070007u) | 0x64006400u, n0);
-      pr[5 * p + 1] = pk_add_f16((w[p] & 0x00380038u) | 0x58005800u, n3);
-      pr[5 * p + 2] = pk_add_f16((w[p] & 0x01C001C0u) | 0x4C004C00u, n6);
-      pr[5 * p + 3] = pk_add_f16((t & 0x00070007u) | 0x64006400u, n0);
-      pr[5 * p + 4] = pk_add_f16((t & 0x00380038u) | 0x58005800u, n3);
+      pr[5 * p + 0] = pk_add_f16(and_or(w[p], 0x00070007u, 0x64006400u), n0);
+      pr[5 * p + 1] = pk_add_f16(and_or(w[p], 0x00380038u, 0x58005800u), n3);
+      pr[5 * p + 2] = pk_add_f16(and_or(w[p], 0x01C001C0u, 0x4C004C00u), n6);
+      pr[5 * p + 3] = pk_add_f16(and_or(t, 0x00070007u, 0x64006400u), n0);
+      pr[5 * p + 4] = pk_add_f16(and_or(t, 0x00380038u, 0x58005800u), n3);
     }
     // codes 30/31: code bit j is bit 9 / bit 25 of plane j -> field at bits 7-9
     const uint32_t spare = ((w[0] >> 2) & 0x00800080u) | ((w[1] >> 1) & 0x01000100u) | (w[2] & 0x02000200u);
@@ -71,10 +85,10 @@ __device__ __forceinline__ void unpack_chunk_exact(const uint32_t (&w)[BITS], ui
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       const uint32_t t = w[p] >> 8;
-      pr[4 * p + 0] = pk_add_f16((w[p] & 0x000F000Fu) | 0x64006400u, n0);
-      pr[4 * p + 1] = pk_add_f16((w[p] & 0x00F000F0u) | 0x54005400u, n4);
-      pr[4 * p + 2] = pk_add_f16((t & 0x000F000Fu) | 0x64006400u, n0);
-      pr[4 * p + 3] = pk_add_f16((t & 0x00F000F0u) | 0x54005400u, n4);
+      pr[4 * p + 0] = pk_add_f16(and_or(w[p], 0x000F000Fu, 0x64006400u), n0);
+      pr[4 * p + 1] = pk_add_f16(and_or(w[p], 0x00F000F0u, 0x54005400u), n4);
+      pr[4 * p + 2] = pk_add_f16(and_or(t, 0x000F000Fu, 0x64006400u), n0);
+      pr[4 * p + 3] = pk_add_f16(and_or(t, 0x00F000F0u, 0x54005400u), n4);
     }
   }
 }
@@ -122,7 +136,7 @@ __device__ __forceinline__ void mfma_block(
   const int K = 128 * G;
   const int W = (int)(blockDim.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar loop
   const int nl = lane & 15;  // weight row of a tile / activation row / result column
   const int q = lane >> 4;   // load: group of the quad; compute: chunk of the group
   const int64_t row0 = (int64_t)block * (16 * TW);
@@ -225,6 +239,170 @@ __device__ __forceinline__ void mfma_block(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Activation-sharing variant for many row tiles.  A block of TB waves owns TB
+// consecutive 16-row tiles, one per wave, and walks K one quad (4 groups =
+// 512 columns) at a time.  The quad's activation slab x[0..15][512q ..
+// 512q+511] (rows past M read as zero) goes straight from memory into LDS
+// (16-byte direct-to-LDS buffer loads, no registers), once per block for its
+// TB tiles, into one of three buffers: the slab of quad q+2 is requested
+// while quad q is computed.  A wave's weights for quad q+1 are requested
+// before quad q is computed; per lane and quad they are the loads of
+// mfma_block (row n, group 4q + j, one 16-byte load per plane).  One barrier
+// per quad.
+//
+// Slab rows are 64 pieces of 16 bytes; piece p of row m sits at position
+// p ^ (m & 7), so the A-fragment reads of a wave (16 rows x 4 pieces) spread
+// over all LDS banks.  Lane l of a direct load writes position l, so it
+// fetches piece l ^ (m & 7).
+// ---------------------------------------------------------------------------
+constexpr int kSlabBuffers = 3;
+constexpr uint32_t kSlabBytes = 16 * 64 * 16;
+constexpr uint32_t kSlabLdsBytes = kSlabBuffers * kSlabBytes;
+
+struct QuadWeights3 {
+  u32x4 w[3];
+  uint32_t s, z;
+};
+struct QuadWeights4 {
+  u32x4 w[4];
+  uint32_t s, z;
+};
+template <int BITS>
+using QuadWeights = typename std::conditional<BITS == 3, QuadWeights3, QuadWeights4>::type;
+
+// Loads of one quad for lane (n, j); groups past G (and idle tiles, whose
+// extents are zero) read zeros.  BITS + 2 vector-memory instructions.
+template <int BITS>
+__device__ __forceinline__ QuadWeights<BITS> load_quad(__amdgpu_buffer_rsrc_t qr, __amdgpu_buffer_rsrc_t sr,
+                                                       __amdgpu_buffer_rsrc_t zr, int n, int j, int q, int G,
+                                                       bool live) {
+  QuadWeights<BITS> r;
+  const int C = 4 * G;
+  const int gq = 4 * q + j;
+  const bool ok = live && gq < G;
+#pragma unroll
+  for (int p = 0; p < BITS; ++p)
+    r.w[p] = __builtin_amdgcn_raw_buffer_load_b128(qr, ok ? (uint32_t)(((n * BITS + p) * C + 4 * gq) * 4) : kOffsetNone,
+                                                   0, kStreamPolicyM);
+  r.s = __builtin_amdgcn_raw_buffer_load_b16(sr, ok ? (uint32_t)(n * G + gq) * 2 : kOffsetNone, 0, 0);
+  r.z = __builtin_amdgcn_raw_buffer_load_b8(zr, ok ? (uint32_t)(n * G + gq) : kOffsetNone, 0, 0);
+  return r;
+}
+
+template <int BITS, int TB>
+__device__ __forceinline__ void mfma_tiles_block(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
+  extern __shared__ u32x4 slab[];  // [kSlabBuffers][16 rows][64 pieces]
+  constexpr int XL = 16 / TB;      // slab rows (direct loads) per wave and quad
+  constexpr int WL = BITS + 2;     // weight loads per lane and quad
+  const int K = 128 * G;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar descriptors
+  const int nl = lane & 15;  // weight row / activation row / result column
+  const int j = lane >> 4;   // load: group of the quad; compute: chunk of the group
+  const int nq = (G + 3) >> 2;
+  const int64_t row0 = ((int64_t)block * TB + wave) * 16;
+  const int rows = (int)max((int64_t)0, min((int64_t)16, (int64_t)N - row0));
+
+  const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
+  const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * 4 * G, (uint32_t)rows * BITS * G * 16);  // 16 B per plane-group
+  const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
+  const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
+
+  // Slab of quad qq into buffer qq % 3: wave w fetches rows w, w + TB, ...;
+  // rows m >= M, columns past K and quads past the last read zeros.
+  auto fetch_slab = [&](int qq) {
+    typedef __attribute__((address_space(3))) void lds_void;
+    const int buf = qq % kSlabBuffers;
+#pragma unroll
+    for (int i = 0; i < XL; ++i) {
+      const int m = wave + i * TB;
+      const int piece = lane ^ (m & 7);
+      const int col = 512 * qq + 8 * piece;
+      const bool ok = m < M && qq < nq && col < K;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(slab + (buf * 16 + m) * 64), 16,
+                                               ok ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
+    }
+  };
+
+  // Issue order X0, W0, X1: waiting until only X1 is outstanding completes
+  // X0 (this wave's part of the slab) and W0.
+  fetch_slab(0);
+  QuadWeights<BITS> cur = load_quad<BITS>(qr, sr, zr, nl, j, 0, G, true);
+  fetch_slab(1);
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (XL & 15) | (((XL >> 4) & 3) << 14));
+  __syncthreads();
+
+  float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < nq; ++q) {
+    // Quad q + 2's slab, then quad q + 1's weights (loads past the last quad
+    // read zeros; the slab buffer written here was last read in quad q - 1).
+    fetch_slab(q + 2);
+    QuadWeights<BITS> nxt = load_quad<BITS>(qr, sr, zr, nl, j, q + 1, G, q + 1 < nq);
+    __builtin_amdgcn_sched_barrier(0);
+
+    // Quarter transposes: chunk j of group 4q + gi in component gi.
+    uint32_t wt[BITS][4];
+#pragma unroll
+    for (int p = 0; p < BITS; ++p) {
+      wt[p][0] = cur.w[p][0];
+      wt[p][1] = cur.w[p][1];
+      wt[p][2] = cur.w[p][2];
+      wt[p][3] = cur.w[p][3];
+      transpose_quarters(wt[p][0], wt[p][1], wt[p][2], wt[p][3]);
+    }
+    uint32_t szj[4];
+    szj[0] = szj[1] = szj[2] = szj[3] = cur.s | (cur.z << 16);
+    transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
+
+    const u32x4* sl = slab + ((q % kSlabBuffers) * 16 + nl) * 64;
+    const int swz = nl & 7;
+#pragma unroll
+    for (int gi = 0; gi < 4; ++gi) {
+      uint32_t w[BITS];
+#pragma unroll
+      for (int p = 0; p < BITS; ++p) w[p] = wt[p][gi];
+      uint32_t pr[16];
+      unpack_chunk_exact<BITS>(w, szj[gi] >> 16, pr);
+      float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const half8_t a = __builtin_bit_cast(half8_t, sl[(16 * gi + 4 * j + jj) ^ swz]);
+        const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+      }
+      const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[gi] & 0xFFFFu));
+      yacc += s * c;
+    }
+
+    // Quad q + 1's slab (requested one quad ago, before the weights of this
+    // quad's successor) is complete when at most this quad's XL + WL loads
+    // are outstanding; then the barrier publishes it to every wave.
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0x0F70 | ((XL + WL) & 15) | ((((XL + WL) >> 4) & 3) << 14));
+    __syncthreads();
+    cur = nxt;
+  }
+
+  // Lane (n, j) holds rows m = 4j .. 4j+3 of column n.
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int m = 4 * j + r;
+    if (m < M && nl < rows) y[(int64_t)m * N + row0 + nl] = __builtin_bit_cast(uint16_t, (_Float16)yacc[r]);
+  }
+}
+
+template <int BITS, int TB>
+__global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
+  const int block = xcd_block();
+  if (block >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
+  mfma_tiles_block<BITS, TB>(x, qw, scales, zeros, y, M, N, G, block);
+}
+
 template <int BITS, int TW>
 __global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
@@ -260,6 +438,23 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   // (the fragments then outweigh the weights) and there are enough tiles to
   // keep a block on every compute unit (measured on MI355X).
   const int64_t tiles = (N + 15) / 16;
+  // Many tiles: blocks of four tiles share each activation slab through LDS.
+  // Blocks of four tiles fit three to a compute unit (LDS), so up to 768
+  // blocks are resident at once; from 3072 tiles on, blocks of eight (two to a
+  // compute unit).
+  if (tune.mfma_tiles == 0 && tiles >= tune.mfma_share_min_tiles) {
+    const int tb = tiles >= 3072 ? 8 : 4;
+    const int nblocks = (int)((tiles + tb - 1) / tb);
+    tune.last_blocks = nblocks;
+    tune.last_rows = 16 * tb;
+    if (tb == 8)
+      launch(linear_mfma_tiles_kernel<BITS, 8>, dim3(xcd_grid(nblocks)), dim3(512), kSlabLdsBytes, stream, ev, x,
+             qweight, scales, zeros, y, M, (int)N, G, nblocks);
+    else
+      launch(linear_mfma_tiles_kernel<BITS, 4>, dim3(xcd_grid(nblocks)), dim3(256), kSlabLdsBytes, stream, ev, x,
+             qweight, scales, zeros, y, M, (int)N, G, nblocks);
+    return hipGetLastError();
+  }
   const int TW = tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1);
   // One wave per quad of the row, at most 16 / TW (register budget; longer
   // rows loop).

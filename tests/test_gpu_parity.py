@@ -381,6 +381,23 @@ def test_matrix_core_two_tiles_ragged(bits):
         assert r["ok"], (M, r)
 
 
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("N,K", [(16404, 640), (16400, 128), (16448, 2560)])
+def test_matrix_core_shared_slab(bits, N, K):
+    """Enough 16-row tiles (>= 1024) for blocks of four tiles sharing each
+    activation slab through LDS: a last block with a partial tile and idle
+    waves (N = 16404 = 1025 * 16 + 4), a partial last 4-group quad (K = 640,
+    five groups) and a single group (K = 128), and M from 2 to 16."""
+    say("mfma shared slab", bits, N, K)
+    w = inputs.weights(N, K, cfg=17, layer=bits, proj=K % 97)
+    codes, qw, s, z = oracle_packed(w, bits)
+    for M in (2, 3, 5, 8, 16):
+        x = inputs.activations(M, K, cfg=17, layer=M)
+        y = gpu_linear(x, qw, s, z, bits)
+        r = linear_check(y, oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
+
+
 # ---------------------------------------------------------------------------
 # grouped calls: several independent linears in one launch
 # ---------------------------------------------------------------------------
