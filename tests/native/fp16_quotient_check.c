@@ -2,7 +2,7 @@
  * Exhaustive check, over every pair of binary16 operands, that the quotient
  * the quantize kernel forms,
  *     y  = RN(1 / s)                  (one IEEE division per group)
- *     q  = RN(v * y)
+ *     q  = RN(v * y + 0)              (fused; RN(v * y) up to the sign of a zero)
  *     r  = RN(v - q * s)              (fused multiply-add: q * s exact)
  *     q' = RN(q + r * y)              (fused multiply-add)
  * equals the IEEE binary32 quotient RN(v / s) for every finite fp16 v and
@@ -34,7 +34,7 @@ int main(void)
             if (((vb >> 10) & 31) == 31)
                 continue; /* inf / NaN weights are outside the domain */
             const float v = half_to_float((uint16_t)vb);
-            const float q = v * y;
+            const float q = fmaf(v, y, 0.0f); /* RN(v * y) up to the sign of a zero */
             const float r = fmaf(-q, s, v);
             const float q2 = fmaf(r, y, q);
             pairs++;
