@@ -117,21 +117,28 @@ __device__ __forceinline__ void transpose_quarters(uint32_t& r0, uint32_t& r1, u
 
 // Block: TW tiles of 16 weight rows and every group of them.  Work item of a
 // wave: the four consecutive groups 4Q..4Q+3 (a "quad") of all TW tiles; the
-// W waves of the block take quads wave, wave + W, ...  The activation
-// fragments of a quad are loaded once per wave and serve all TW tiles.
+// W waves of the block take quads wave, wave + W, ...
 //
 // Loads of a quad, lane (n = lane % 16, j = lane / 16): per tile, one 16-byte
 // load per plane of row n, group 4Q + j (four chunks), so each row of a tile
 // reads 64 contiguous bytes per plane, and the scale and zero point of that
-// (row, group); once, the activation fragments of the four groups (row m = n
-// of x).  A quarter transpose then gives quarter q chunk q of every group of
-// the quad, the layout the matrix core wants (lane (n, q) supplies row n's
-// codes 32q .. 32q+31 of the group).  Slots past the last group read zeros.
+// (row, group).  The quad's activations x[0..M-1][512Q .. 512Q+511] go into
+// the wave's own LDS slab with 16-byte direct-to-LDS loads, one fully
+// coalesced 1 KiB row piece per instruction (fragment loads straight from
+// memory would touch 64 separate cache lines per instruction); slab rows m >=
+// M are not written and only feed result rows that are not stored.  A
+// quarter transpose then gives quarter q chunk q of every group of the quad,
+// the layout the matrix core wants (lane (n, q) supplies row n's codes 32q ..
+// 32q+31 of the group).  Slots past the last group read zeros.
+constexpr int kWaveSlabU4 = 16 * 64;  // one wave's slab: 16 rows x 64 pieces of 16 bytes
+constexpr int kMaxSlabWaves = 10;     // 160 KiB of LDS per block
+
 template <int BITS, int TW>
 __device__ __forceinline__ void mfma_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
-  extern __shared__ float red[];  // per-wave partial results, [wave][tile][r][lane]
+  typedef __attribute__((address_space(3))) void lds_void;
+  extern __shared__ u32x4 wslabs[];  // [W][16 rows][64 pieces]; afterwards the wave's partials
 
   const int K = 128 * G;
   const int W = (int)(blockDim.x >> 6);
@@ -143,6 +150,8 @@ __device__ __forceinline__ void mfma_block(
   const int rows = (int)min((int64_t)16 * TW, (int64_t)N - row0);
   const int C = 4 * G;
   const int nq = (G + 3) >> 2;
+  u32x4* const sl = wslabs + wave * kWaveSlabU4;
+  const int swz = nl & 7;
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
   const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * C, (uint32_t)rows * BITS * C * 4);
@@ -154,9 +163,15 @@ __device__ __forceinline__ void mfma_block(
   for (int t = 0; t < TW; ++t) yacc[t] = float4_t{0.f, 0.f, 0.f, 0.f};
 
   for (int Q = wave; Q < nq; Q += W) {
-    // 1. Loads.  Rows past the block and x rows m >= M are past their extents.
+    // 1. Loads.  Rows past the block are past their extents.  The slab is
+    //    rewritten only after the previous quad's fragment reads returned.
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    // Groups past G get bit 31 set in their offsets (past every extent):
+    // arithmetic, not a select, which the compiler may turn into a branch
+    // that waits for the loads before it.
     const int gq = 4 * Q + q;
-    const bool okw = gq < G;
+    const uint32_t dead = (uint32_t)(gq >= G) << 31;
     u32x4 wv[TW][BITS];
     uint32_t sraw[TW], zraw[TW];
 #pragma unroll
@@ -165,19 +180,20 @@ __device__ __forceinline__ void mfma_block(
 #pragma unroll
       for (int p = 0; p < BITS; ++p)
         wv[t][p] = __builtin_amdgcn_raw_buffer_load_b128(
-            qr, okw ? (uint32_t)(((nrow * BITS + p) * C + 4 * gq) * 4) : kOffsetNone, 0, kStreamPolicyM);
-      sraw[t] = __builtin_amdgcn_raw_buffer_load_b16(sr, okw ? (uint32_t)(nrow * G + gq) * 2 : kOffsetNone, 0, 0);
-      zraw[t] = __builtin_amdgcn_raw_buffer_load_b8(zr, okw ? (uint32_t)(nrow * G + gq) : kOffsetNone, 0, 0);
+            qr, (uint32_t)(((nrow * BITS + p) * C + 4 * gq) * 4) | dead, 0, kStreamPolicyM);
+      sraw[t] = __builtin_amdgcn_raw_buffer_load_b16(sr, (uint32_t)(nrow * G + gq) * 2 | dead, 0, 0);
+      zraw[t] = __builtin_amdgcn_raw_buffer_load_b8(zr, (uint32_t)(nrow * G + gq) | dead, 0, 0);
     }
-    u32x4 xa[4][4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int g = 4 * Q + j;
-      const uint32_t xo = g < G ? ((uint32_t)nl * (uint32_t)K + (uint32_t)(128 * g + 32 * q)) * 2 : kOffsetNone;
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) xa[j][jj] = __builtin_amdgcn_raw_buffer_load_b128(xr, xo + 16 * jj, 0, 0);
+    // Slab row m: lane l fetches piece l ^ (m & 7) (8 columns) into position
+    // l; columns past K read zero.
+    for (int m = 0; m < M; ++m) {
+      const int col = 512 * Q + 8 * (lane ^ (m & 7));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sl + m * 64), 16,
+                                               col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
     }
-    __builtin_amdgcn_sched_barrier(0);  // every load of the quad goes out before any compute
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): weights and slab
+    __builtin_amdgcn_sched_barrier(0);
 
     // 2. Quarter transposes: plane words (chunk q of group 4Q + j now in
     //    component j) and the four groups' scale | zero << 16 in every quarter.
@@ -201,6 +217,9 @@ __device__ __forceinline__ void mfma_block(
     // 3. Per group and tile: exact (q - z) pairs, four MFMAs, scale.
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
+      half8_t a[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) a[jj] = __builtin_bit_cast(half8_t, sl[nl * 64 + ((16 * j + 4 * q + jj) ^ swz)]);
 #pragma unroll
       for (int t = 0; t < TW; ++t) {
         uint32_t w[BITS];
@@ -211,9 +230,8 @@ __device__ __forceinline__ void mfma_block(
         float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          const half8_t a = __builtin_bit_cast(half8_t, xa[j][jj]);
           const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
-          c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+          c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[jj], b, c, 0, 0, 0);
         }
         const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[t][j] & 0xFFFFu));
         yacc[t] += s * c;
@@ -221,18 +239,21 @@ __device__ __forceinline__ void mfma_block(
     }
   }
 
-  // 4. Fixed-order reduction of the W waves' partials.
+  // 4. Fixed-order reduction of the W waves' partials (each wave's partials
+  //    go into its own slab, whose reads have all returned).
+  float* red = reinterpret_cast<float*>(wslabs);
+  constexpr int kWaveSlabF = kWaveSlabU4 * 4;
 #pragma unroll
   for (int t = 0; t < TW; ++t)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[((wave * TW + t) * 4 + r) * 64 + lane] = yacc[t][r];
+    for (int r = 0; r < 4; ++r) red[wave * kWaveSlabF + (t * 4 + r) * 64 + lane] = yacc[t][r];
   __syncthreads();
   for (int idx = threadIdx.x; idx < TW * 4 * 64; idx += blockDim.x) {
     const int t = idx >> 8;
     const int r = (idx >> 6) & 3;
     const int ln = idx & 63;
     float v = 0.0f;
-    for (int w = 0; w < W; ++w) v += red[((w * TW + t) * 4 + r) * 64 + ln];
+    for (int w = 0; w < W; ++w) v += red[w * kWaveSlabF + (t * 4 + r) * 64 + ln];
     const int m = 4 * (ln >> 4) + r;
     const int n = 16 * t + (ln & 15);
     if (m < M && n < rows) y[(int64_t)m * N + row0 + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
@@ -456,15 +477,15 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
     return hipGetLastError();
   }
   const int TW = tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1);
-  // One wave per quad of the row, at most 16 / TW (register budget; longer
-  // rows loop).
-  const int wmax = 16 / TW;
+  // One wave per quad of the row, at most 16 / TW (register budget) and
+  // kMaxSlabWaves (a 16 KiB activation slab per wave); longer rows loop.
+  const int wmax = min(16 / TW, kMaxSlabWaves);
   const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
   const int nblocks = (int)((tiles + TW - 1) / TW);
   const unsigned blocks = xcd_grid(nblocks);
   tune.last_blocks = nblocks;
   tune.last_rows = 16 * TW;
-  const uint32_t lds = (uint32_t)W * TW * 4 * 64 * 4;
+  const uint32_t lds = (uint32_t)W * kWaveSlabU4 * 16;
   if (TW == 2)
     launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
            (int)N, G, nblocks);
@@ -490,9 +511,9 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
   }
   grp.count = count;
   grp.blocks = (int)blocks;
-  const int W = min(16, nq_max);
-  launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * 4 * 64 * 4, stream, ev,
-         grp, M);
+  const int W = min(kMaxSlabWaves, nq_max);
+  launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * kWaveSlabU4 * 16, stream,
+         ev, grp, M);
   return hipGetLastError();
 }
 
