@@ -305,7 +305,8 @@ def cpu_baseline(budget_s=12.0):
 def profile_run(args, dev):
     """Workload for counter collection: a plain device copy of known size
     (its FETCH_SIZE / WRITE_SIZE calibrate the counters) followed by eager
-    steps of the W3 M=1 stack (one dispatch per linear call)."""
+    steps of the W3 stack at M = --profile-m activation rows (one dispatch
+    per linear call)."""
     import torch
     nbytes = 256 << 20
     a = torch.empty(nbytes // 2, dtype=torch.float16, device=dev).fill_(1.0)
@@ -316,10 +317,10 @@ def profile_run(args, dev):
     del a, b
     stack = Stack(args.workload, dev, bits_list=(3,), fused=not args.unfused)
     for _ in range(args.steps):
-        stack.step(1, 3)
+        stack.step(args.profile_m, 3)
     torch.cuda.synchronize()
-    print("profile run: copy 3 x %d bytes; %d steps x %d linear calls; %d weight bytes per step"
-          % (nbytes, args.steps, len(stack.shapes), int(stack.weight_bytes(3))), flush=True)
+    print("profile run: copy 3 x %d bytes; %d steps x %d linear calls at M=%d; %d weight bytes per step"
+          % (nbytes, args.steps, len(stack.shapes), args.profile_m, int(stack.weight_bytes(3))), flush=True)
 
 
 def main():
@@ -334,6 +335,7 @@ def main():
     ap.add_argument("--profile-run", action="store_true",
                     help="for rocprofv3: a 256 MiB device copy (counter calibration) and --steps eager "
                          "W3 M=1 stack steps; prints a short summary instead of the JSON line")
+    ap.add_argument("--profile-m", type=int, default=1, help="activation rows of the --profile-run steps (1..16)")
     ap.add_argument("--unfused", action="store_true",
                     help="one call per projection (7 per layer) instead of one per shared-input stage (4)")
     args = ap.parse_args()
