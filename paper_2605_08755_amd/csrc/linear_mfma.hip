@@ -424,6 +424,112 @@ __global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
   mfma_tiles_block<BITS, TB>(x, qw, scales, zeros, y, M, N, G, block);
 }
 
+// ---------------------------------------------------------------------------
+// Rows of at most five quads (K <= 2560) with many row tiles: one memory
+// round trip per wave.  A block of four waves owns four 16-row tiles, one per
+// wave, and requests everything at once: the activation slabs of all NQ quads
+// (each slab once per block, x[0..M-1][512q .. 512q+511] into LDS by
+// direct-to-LDS loads, four rows per wave) and the wave's weights of all NQ
+// quads (registers).  After one wait and one barrier the wave computes its
+// tile's NQ quads.  The walk-one-quad-at-a-time kernel above pays one round
+// trip per quad instead (its prefetch is one quad ahead, and a quad's compute
+// is far shorter than a round trip).  Slab rows m >= M are not written and
+// only feed result rows that are not stored.
+// ---------------------------------------------------------------------------
+constexpr int kFullTiles = 4;
+
+template <int BITS, int NQ>
+__device__ __forceinline__ void mfma_full_block(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  extern __shared__ u32x4 slab[];  // [NQ][16 rows][64 pieces]
+  const int K = 128 * G;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar descriptors
+  const int nl = lane & 15;  // weight row / activation row / result column
+  const int j = lane >> 4;   // load: group of the quad; compute: chunk of the group
+  const int64_t row0 = ((int64_t)block * kFullTiles + wave) * 16;
+  const int rows = (int)max((int64_t)0, min((int64_t)16, (int64_t)N - row0));
+
+  const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
+  const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * 4 * G, (uint32_t)rows * BITS * G * 16);
+  const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
+  const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
+
+  // 1. Every load of the block: slab rows wave, wave + 4, ... (< M) of each
+  //    quad, then the wave's weights of each quad.  Columns past K and groups
+  //    past G read zeros.
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    for (int m = wave; m < M; m += kFullTiles) {
+      const int col = 512 * q + 8 * (lane ^ (m & 7));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(slab + (q * 16 + m) * 64), 16,
+                                               col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
+    }
+  }
+  QuadWeights<BITS> wq[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) wq[q] = load_quad<BITS>(qr, sr, zr, nl, j, q, G, true);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  __syncthreads();
+
+  // 2. The tile's quads.
+  float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
+  const int swz = nl & 7;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    // Quarter transposes: chunk j of group 4q + gi in component gi.
+    uint32_t wt[BITS][4];
+#pragma unroll
+    for (int p = 0; p < BITS; ++p) {
+      wt[p][0] = wq[q].w[p][0];
+      wt[p][1] = wq[q].w[p][1];
+      wt[p][2] = wq[q].w[p][2];
+      wt[p][3] = wq[q].w[p][3];
+      transpose_quarters(wt[p][0], wt[p][1], wt[p][2], wt[p][3]);
+    }
+    uint32_t szj[4];
+    szj[0] = szj[1] = szj[2] = szj[3] = wq[q].s | (wq[q].z << 16);
+    transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
+
+    const u32x4* sl = slab + (q * 16 + nl) * 64;
+#pragma unroll
+    for (int gi = 0; gi < 4; ++gi) {
+      uint32_t w[BITS];
+#pragma unroll
+      for (int p = 0; p < BITS; ++p) w[p] = wt[p][gi];
+      uint32_t pr[16];
+      unpack_chunk_exact<BITS>(w, szj[gi] >> 16, pr);
+      float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const half8_t a = __builtin_bit_cast(half8_t, sl[(16 * gi + 4 * j + jj) ^ swz]);
+        const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+      }
+      const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[gi] & 0xFFFFu));
+      yacc += s * c;
+    }
+  }
+
+  // 3. Lane (n, j) holds rows m = 4j .. 4j+3 of column n.
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int m = 4 * j + r;
+    if (m < M && nl < rows) y[(int64_t)m * N + row0 + nl] = __builtin_bit_cast(uint16_t, (_Float16)yacc[r]);
+  }
+}
+
+template <int BITS, int NQ>
+__global__ __launch_bounds__(64 * kFullTiles) void linear_mfma_full_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
+  const int block = xcd_block();
+  if (block >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
+  mfma_full_block<BITS, NQ>(x, qw, scales, zeros, y, M, N, G, block);
+}
+
 template <int BITS, int TW>
 __global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
@@ -463,6 +569,21 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   // Blocks of four tiles fit three to a compute unit (LDS), so up to 768
   // blocks are resident at once; from 3072 tiles on, blocks of eight (two to a
   // compute unit).
+  if (tune.mfma_tiles == 0 && tiles >= tune.mfma_share_min_tiles && nq <= 5) {
+    const int nblocks = (int)((tiles + kFullTiles - 1) / kFullTiles);
+    tune.last_blocks = nblocks;
+    tune.last_rows = 16 * kFullTiles;
+    const dim3 grid(xcd_grid(nblocks)), blk(64 * kFullTiles);
+    const uint32_t lds = (uint32_t)nq * kSlabBytes;
+    switch (nq) {
+      case 1: launch(linear_mfma_full_kernel<BITS, 1>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
+      case 2: launch(linear_mfma_full_kernel<BITS, 2>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
+      case 3: launch(linear_mfma_full_kernel<BITS, 3>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
+      case 4: launch(linear_mfma_full_kernel<BITS, 4>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
+      default: launch(linear_mfma_full_kernel<BITS, 5>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
+    }
+    return hipGetLastError();
+  }
   if (tune.mfma_tiles == 0 && tiles >= tune.mfma_share_min_tiles) {
     const int tb = tiles >= 3072 ? 8 : 4;
     const int nblocks = (int)((tiles + tb - 1) / tb);

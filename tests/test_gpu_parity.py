@@ -384,10 +384,11 @@ def test_matrix_core_two_tiles_ragged(bits):
 @pytest.mark.parametrize("bits", [3, 4])
 @pytest.mark.parametrize("N,K", [(16404, 640), (16400, 128), (16448, 2560)])
 def test_matrix_core_shared_slab(bits, N, K):
-    """Enough 16-row tiles (>= 1024) for blocks of four tiles sharing each
-    activation slab through LDS: a last block with a partial tile and idle
-    waves (N = 16404 = 1025 * 16 + 4), a partial last 4-group quad (K = 640,
-    five groups) and a single group (K = 128), and M from 2 to 16."""
+    """Enough 16-row tiles (>= 1024) for blocks of four tiles sharing the
+    activation slabs through LDS (K <= 2560: all quads in one round trip): a
+    last block with a partial tile and idle waves (N = 16404 = 1025 * 16 + 4),
+    a partial last 4-group quad (K = 640, five groups) and a single group
+    (K = 128), and M from 2 to 16."""
     say("mfma shared slab", bits, N, K)
     w = inputs.weights(N, K, cfg=17, layer=bits, proj=K % 97)
     codes, qw, s, z = oracle_packed(w, bits)
@@ -396,6 +397,32 @@ def test_matrix_core_shared_slab(bits, N, K):
         y = gpu_linear(x, qw, s, z, bits)
         r = linear_check(y, oracle.linear(x, codes, s, z))
         assert r["ok"], (M, r)
+
+
+def test_matrix_core_walk_ragged():
+    """From 3072 row tiles, blocks of eight tiles walk K one quad at a time
+    (K > 2560): N = 49168 = 3073 * 16 (a last block with one tile), K = 3200
+    (25 groups: a partial last quad).  Quantize on the GPU; codes and outputs
+    checked on sampled rows and the last rows."""
+    N, K = 49168, 3200
+    say("mfma walk ragged", N, K)
+    rng = np.random.default_rng(49)
+    w = inputs.weights(N, K, cfg=18, layer=3, proj=7)
+    rows = np.concatenate([np.sort(rng.choice(N - 16, 80, replace=False)), np.arange(N - 16, N)])
+    codes, qw, s, z = oracle_packed(np.ascontiguousarray(w[rows]), 3)
+    wd = to_dev(w)
+    q, sd, zd = laq.quantize(wd, 3)
+    del wd
+    torch.cuda.synchronize()
+    assert np.array_equal(q[rows].cpu().numpy().view(np.uint32), qw)
+    for M in (3, 8, 16):
+        x = inputs.activations(M, K, cfg=18, layer=M)
+        y = laq.linear(to_dev(x), q, sd, zd, 3)
+        torch.cuda.synchronize()
+        r = linear_check(y.cpu().numpy()[:, rows], oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
+    del q, sd, zd
+    torch.cuda.empty_cache()
 
 
 # ---------------------------------------------------------------------------
