@@ -25,7 +25,8 @@
  * ---------------------------------
  *  - Tensor pointers are DEVICE pointers into memory the caller owns and
  *    keeps alive until the stream work completes.  The library never
- *    allocates, frees or synchronizes inside these calls.
+ *    allocates, frees or synchronizes inside these calls (scratch memory,
+ *    where a call can use it, is a caller-provided workspace).
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Work is enqueued asynchronously; results are valid once the caller
  *    synchronizes with the stream.
@@ -165,6 +166,46 @@ laq_status laq_linear_w3g128(const void *x, const uint32_t *qweight,
                              void *stream);
 
 /*
+ * laq_linear_workspace_bytes -- device workspace (bytes) with which
+ * laq_linear_ws_w3g128 / laq_linear_ws_w4g128 split K across workgroups for
+ * an (M, N, K) call: the reduction along K of Eq. 1's dot products, which
+ * App. G's GEMV spreads over a 2-D grid of thread blocks, here deterministic
+ * (fp32 partial sums per K range, added in a fixed order by a second kernel).
+ * It applies on the matrix-core path (M >= 2) to rows of at least 40 quads
+ * of four groups (K > 19968) and fewer than 1024 tiles of 16 rows
+ * (N <= 16368): there, four tiles per workgroup share each activation slab
+ * and the K ranges give every compute unit work, which outweighs the second
+ * kernel (measured on MI355X: Qwen3-32B down projection, N = 5120,
+ * K = 25600, M = 16: 33.2 -> 31.3 us; shorter rows measured slower split).  Returns 0 when the call
+ * never splits K (then the _ws entry point is the plain one), otherwise an
+ * upper bound of what the call uses.  Depends on the shape only (not on the
+ * bit width); an invalid shape gives 0.
+ */
+int64_t laq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
+ * laq_linear_ws_w3g128 -- laq_linear_w3g128 with a caller-provided workspace.
+ *
+ *   workspace        [scratch] device memory, 16-byte aligned, any contents;
+ *                    the call writes and reads it (fp32 partial sums).  It
+ *                    must overlap no other argument and serve no other call
+ *                    in flight (one workspace per stream).  May be NULL when
+ *                    workspace_bytes is 0.
+ *   workspace_bytes  [in] its size.  With workspace_bytes >=
+ *                    laq_linear_workspace_bytes(M, N, K) > 0 the call splits
+ *                    K; otherwise it is laq_linear_w3g128.
+ *
+ * Results: within the linear tolerance of laq_linear_w3g128 (the fp32 sums
+ * are added in another order), bitwise-identical from call to call for the
+ * same shape.  The call enqueues two kernels when it splits K.
+ */
+laq_status laq_linear_ws_w3g128(const void *x, const uint32_t *qweight,
+                                const void *scales, const uint8_t *zeros,
+                                void *y, int64_t M, int64_t N, int64_t K,
+                                void *workspace, int64_t workspace_bytes,
+                                void *stream);
+
+/*
  * laq_linear_group_w3g128 -- several independent laq_linear_w3g128 calls
  * (1 <= count <= LAQ_MAX_GROUP) with the same M, issued as one kernel launch:
  * for instance the q, k and v projections of a decoder layer, which read the
@@ -214,6 +255,12 @@ laq_status laq_linear_w4g128(const void *x, const uint32_t *qweight,
                              const void *scales, const uint8_t *zeros,
                              void *y, int64_t M, int64_t N, int64_t K,
                              void *stream);
+
+laq_status laq_linear_ws_w4g128(const void *x, const uint32_t *qweight,
+                                const void *scales, const uint8_t *zeros,
+                                void *y, int64_t M, int64_t N, int64_t K,
+                                void *workspace, int64_t workspace_bytes,
+                                void *stream);
 
 #ifdef __cplusplus
 }

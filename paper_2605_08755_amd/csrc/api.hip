@@ -92,6 +92,28 @@ laq_status linear(const char* fn, const void* x, const uint32_t* qweight, const 
 }
 
 template <int BITS>
+laq_status linear_ws(const char* fn, const void* x, const uint32_t* qweight, const void* scales,
+                     const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* workspace,
+                     int64_t workspace_bytes, void* stream) {
+  const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
+  if (!x || !qweight || !scales || !zeros || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  if (workspace_bytes < 0) return fail(LAQ_ERR_BAD_SHAPE, fn, "workspace_bytes must be >= 0");
+  if (workspace_bytes > 0 && !workspace) return fail(LAQ_ERR_NULL_POINTER, fn, "null workspace with workspace_bytes > 0");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (M < 1 || M > LAQ_MAX_M) return fail(LAQ_ERR_BAD_M, fn, "M must be in 1..16");
+  if (!aligned(x, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "x and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  if (workspace && !aligned(workspace, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "workspace must be 16-byte aligned");
+  return hip_status(fn, laq::launch_linear<BITS>(static_cast<const uint16_t*>(x), qweight,
+                                                 static_cast<const uint16_t*>(scales), zeros,
+                                                 static_cast<uint16_t*>(y), (int)M, N, K,
+                                                 static_cast<hipStream_t>(stream), ev,
+                                                 workspace_bytes > 0 ? static_cast<float*>(workspace) : nullptr,
+                                                 (size_t)workspace_bytes));
+}
+
+template <int BITS>
 laq_status linear_group(const char* fn, const laq_linear_call* calls, int32_t count, int64_t M, void* stream) {
   const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
   if (!calls) return fail(LAQ_ERR_NULL_POINTER, fn, "null calls array");
@@ -164,6 +186,28 @@ laq_status laq_linear_w3g128(const void* x, const uint32_t* qweight, const void*
                              const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
                              void* stream) {
   return linear<3>("laq_linear_w3g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+int64_t laq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M < 1 || M > LAQ_MAX_M || N < 1 || N > 0x7FFFFFFFLL || K < 128 || K % 128 != 0 || K > (1LL << 24) ||
+      N * K >= (1LL << 40))
+    return 0;
+  const laq::SplitPlan p = laq::mfma_split_plan((int)M, N, (int)(K / 128));
+  return (int64_t)laq::split_workspace_bytes(p, (int)M, N);
+}
+
+laq_status laq_linear_ws_w3g128(const void* x, const uint32_t* qweight, const void* scales,
+                                const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                                void* workspace, int64_t workspace_bytes, void* stream) {
+  return linear_ws<3>("laq_linear_ws_w3g128", x, qweight, scales, zeros, y, M, N, K, workspace, workspace_bytes,
+                      stream);
+}
+
+laq_status laq_linear_ws_w4g128(const void* x, const uint32_t* qweight, const void* scales,
+                                const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                                void* workspace, int64_t workspace_bytes, void* stream) {
+  return linear_ws<4>("laq_linear_ws_w4g128", x, qweight, scales, zeros, y, M, N, K, workspace, workspace_bytes,
+                      stream);
 }
 
 laq_status laq_linear_group_w3g128(const laq_linear_call* calls, int32_t count, int64_t M, void* stream) {

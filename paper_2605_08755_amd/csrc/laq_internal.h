@@ -57,6 +57,7 @@ struct LinearTuning {
   int mfma_waves = 0;        // matrix-core kernel: waves per block (1..16); 0 = one per group quad
   int mfma_tiles = 0;        // matrix-core kernel: 16-row tiles per block (1 or 2); 0 = chosen from N
   int mfma_share_min_tiles = 1024;  // from this many 16-row tiles: four tiles per block share the activations
+  int split_min_quads = 40;         // fewer tiles: K is split (given a workspace) from rows of this many quads
 };
 LinearTuning& linear_tuning();
 
@@ -89,10 +90,28 @@ template <int BITS>
 hipError_t launch_pack(const uint16_t* w, const uint16_t* scales, const uint8_t* zeros, int64_t N,
                        int64_t K, uint32_t* qweight, hipStream_t stream, const LaunchEvents& ev);
 
+// Split K on the matrix-core path for fewer than mfma_share_min_tiles row
+// tiles and rows of at least split_min_quads quads: S K ranges of qs quads,
+// tile_blocks blocks of four tiles per range; S == 1 means no split.  A pure
+// function of the shape (and the tuning).
+struct SplitPlan {
+  int S = 1;
+  int qs = 0;
+  int tile_blocks = 0;
+};
+SplitPlan mfma_split_plan(int M, int64_t N, int G);
+// fp32 partial sums [S][M][N].
+inline size_t split_workspace_bytes(const SplitPlan& p, int M, int64_t N) {
+  return p.S > 1 ? (size_t)p.S * (size_t)M * (size_t)N * sizeof(float) : 0;
+}
+
+// workspace: device memory of workspace_bytes for the split-K partial sums,
+// or null (then K is not split).
 template <int BITS>
 hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                               const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
-                              hipStream_t stream, const LaunchEvents& ev);
+                              hipStream_t stream, const LaunchEvents& ev, float* workspace,
+                              size_t workspace_bytes);
 
 // calls[i].{x, qw, scales, zeros, y, N, G} filled in by the caller; count in 1..kMaxGroup.
 template <int BITS>
@@ -105,6 +124,7 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
-                         hipStream_t stream, const LaunchEvents& ev);
+                         hipStream_t stream, const LaunchEvents& ev, float* workspace = nullptr,
+                         size_t workspace_bytes = 0);
 
 }  // namespace laq

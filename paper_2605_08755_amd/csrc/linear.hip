@@ -452,14 +452,15 @@ LinearTuning& linear_tuning() {
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
-                         hipStream_t stream, const LaunchEvents& ev) {
+                         hipStream_t stream, const LaunchEvents& ev, float* workspace,
+                         size_t workspace_bytes) {
   const int G = (int)(K / 128);
   const int MT = ceil_pow2(M);
   // Matrix cores from mfma_min_m rows on, except that the VALU kernel stays
   // ahead up to 4 rows when rows are short (measured on MI355X: it re-reads
   // the activations from LDS per unit, which costs more as rows get longer).
   if (M >= linear_tuning().mfma_min_m && !(M <= 4 && G <= 24))
-    return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev);
+    return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev, workspace, workspace_bytes);
   const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
   {
@@ -512,7 +513,8 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   }
   // Activation tile too large for the flat kernel's LDS: matrix cores for
   // several rows, the K-tiled kernel below for one.
-  if (M >= 2) return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev);
+  if (M >= 2)
+    return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev, workspace, workspace_bytes);
   // Lanes per row: enough that one K tile covers the row in a few groups per
   // lane, then more while the grid is small, capped by the row's group count.
   int L = 4;
@@ -606,9 +608,9 @@ template hipError_t launch_linear_group<3>(LinearCall*, int, int, hipStream_t, c
 template hipError_t launch_linear_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
                                      uint16_t*, int, int64_t, int64_t, hipStream_t,
-                                     const LaunchEvents&);
+                                     const LaunchEvents&, float*, size_t);
 template hipError_t launch_linear<4>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
                                      uint16_t*, int, int64_t, int64_t, hipStream_t,
-                                     const LaunchEvents&);
+                                     const LaunchEvents&, float*, size_t);
 
 }  // namespace laq

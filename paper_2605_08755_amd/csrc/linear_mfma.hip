@@ -448,10 +448,14 @@ __global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kFullTiles = 4;
 
+// Quads q0 .. q0+NQ-1 (those past the row read zeros).  part == nullptr: the
+// result goes to y as fp16; otherwise the fp32 partial sums go to
+// part[m][n] (split K).
 template <int BITS, int NQ>
 __device__ __forceinline__ void mfma_full_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block, int q0,
+    float* __restrict__ part) {
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ u32x4 slab[];  // [NQ][16 rows][64 pieces]
   const int K = 128 * G;
@@ -473,14 +477,14 @@ __device__ __forceinline__ void mfma_full_block(
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     for (int m = wave; m < M; m += kFullTiles) {
-      const int col = 512 * q + 8 * (lane ^ (m & 7));
+      const int col = 512 * (q0 + q) + 8 * (lane ^ (m & 7));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(slab + (q * 16 + m) * 64), 16,
                                                col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
     }
   }
   QuadWeights<BITS> wq[NQ];
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) wq[q] = load_quad<BITS, kWeightPolicyNT>(qr, sr, zr, nl, j, q, G, true);
+  for (int q = 0; q < NQ; ++q) wq[q] = load_quad<BITS, kWeightPolicyNT>(qr, sr, zr, nl, j, q0 + q, G, true);
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   __syncthreads();
 
@@ -527,7 +531,10 @@ __device__ __forceinline__ void mfma_full_block(
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int m = 4 * j + r;
-    if (m < M && nl < rows) y[(int64_t)m * N + row0 + nl] = __builtin_bit_cast(uint16_t, (_Float16)yacc[r]);
+    if (m < M && nl < rows) {
+      if (part) part[(int64_t)m * N + row0 + nl] = yacc[r];
+      else y[(int64_t)m * N + row0 + nl] = __builtin_bit_cast(uint16_t, (_Float16)yacc[r]);
+    }
   }
 }
 
@@ -537,7 +544,58 @@ __global__ __launch_bounds__(64 * kFullTiles) void linear_mfma_full_kernel(
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
   const int block = xcd_block();
   if (block >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
-  mfma_full_block<BITS, NQ>(x, qw, scales, zeros, y, M, N, G, block);
+  mfma_full_block<BITS, NQ>(x, qw, scales, zeros, y, M, N, G, block, 0, nullptr);
+}
+
+// Split K: logical block b = s * tile_blocks + t takes tile block t over the
+// quads s * NQ .. s * NQ + NQ - 1 and writes its partial sums to part[s][M][N]
+// (consecutive blocks share a K range, i.e. the activation columns, in L2).
+template <int BITS, int NQ>
+__global__ __launch_bounds__(64 * kFullTiles) void linear_mfma_split_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, float* __restrict__ part, int M, int N, int G, int tile_blocks,
+    int nblocks) {
+  const int b = xcd_block();
+  if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
+  const int sidx = b / tile_blocks;
+  mfma_full_block<BITS, NQ>(x, qw, scales, zeros, nullptr, M, N, G, b - sidx * tile_blocks, sidx * NQ,
+                            part + (int64_t)sidx * M * N);
+}
+
+// y[i] = fp16 of the sum of the S partials part[s][i], s = 0 .. S-1 in order.
+// Each thread owns four consecutive outputs (16-byte partial loads when
+// M*N is a multiple of 4) and requests eight partials at a time before adding
+// them in order, so the loads of a thread overlap.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                            uint16_t* __restrict__ y, int S, int64_t MN) {
+  const int64_t i0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i0 >= MN) return;
+  float4_t acc;
+  if ((MN & 3) == 0) {
+    const float4_t* p4 = reinterpret_cast<const float4_t*>(part) + (i0 >> 2);
+    const int64_t stride = MN >> 2;
+    acc = p4[0];
+    int s = 1;
+    for (; s + 8 <= S; s += 8) {
+      float4_t v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) v[k] = p4[(int64_t)(s + k) * stride];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc += v[k];
+    }
+    for (; s < S; ++s) acc += p4[(int64_t)s * stride];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = i0 + e < MN ? part[i0 + e] : 0.0f;
+    for (int s = 1; s < S; ++s) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (i0 + e < MN) acc[e] += part[(int64_t)s * MN + i0 + e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (i0 + e < MN) y[i0 + e] = __builtin_bit_cast(uint16_t, (_Float16)acc[e]);
 }
 
 template <int BITS, int TW>
@@ -564,10 +622,27 @@ __global__ __launch_bounds__(1024) void linear_mfma_group_kernel(const LinearGro
 
 }  // namespace
 
+SplitPlan mfma_split_plan(int M, int64_t N, int G) {
+  SplitPlan p;
+  const LinearTuning& tune = linear_tuning();
+  const int64_t tiles = (N + 15) / 16;
+  const int nq = (G + 3) / 4;
+  if (M < 2 || tune.mfma_tiles != 0 || tiles >= tune.mfma_share_min_tiles || nq < tune.split_min_quads) return p;
+  // Blocks of four tiles over K ranges of qs quads: the longest ranges (the
+  // fewest partial sums) that still give every compute unit a block.
+  const int64_t tile_blocks = (tiles + kFullTiles - 1) / kFullTiles;
+  const int64_t smin = (256 + tile_blocks - 1) / tile_blocks;
+  p.qs = (int)min((int64_t)5, max((int64_t)1, (int64_t)nq / smin));
+  p.S = (nq + p.qs - 1) / p.qs;
+  p.tile_blocks = (int)tile_blocks;
+  return p;
+}
+
 template <int BITS>
 hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                               const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
-                              hipStream_t stream, const LaunchEvents& ev) {
+                              hipStream_t stream, const LaunchEvents& ev, float* workspace,
+                              size_t workspace_bytes) {
   const int G = (int)(K / 128);
   LinearTuning& tune = linear_tuning();
   const int nq = (G + 3) / 4;
@@ -605,6 +680,31 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
     else
       launch(linear_mfma_tiles_kernel<BITS, 4>, dim3(xcd_grid(nblocks)), dim3(256), kSlabLdsBytes, stream, ev, x,
              qweight, scales, zeros, y, M, (int)N, G, nblocks);
+    return hipGetLastError();
+  }
+  // Fewer tiles, long rows, a workspace: split K over blocks of four tiles
+  // that request their whole K range at once; a second kernel adds the
+  // ranges' partial sums in order.
+  const SplitPlan sp = mfma_split_plan(M, N, G);
+  if (sp.S > 1 && workspace && workspace_bytes >= split_workspace_bytes(sp, M, N)) {
+    const int nblocks = sp.tile_blocks * sp.S;
+    tune.last_blocks = nblocks;
+    tune.last_rows = 16 * kFullTiles;
+    LaunchEvents e1, e2;  // the measurement hook spans both kernels
+    e1.start = ev.start;
+    e2.stop = ev.stop;
+    const dim3 grid(xcd_grid(nblocks)), blk(64 * kFullTiles);
+    const uint32_t lds = (uint32_t)sp.qs * kSlabBytes;
+    switch (sp.qs) {
+      case 1: launch(linear_mfma_split_kernel<BITS, 1>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
+      case 2: launch(linear_mfma_split_kernel<BITS, 2>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
+      case 3: launch(linear_mfma_split_kernel<BITS, 3>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
+      case 4: launch(linear_mfma_split_kernel<BITS, 4>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
+      default: launch(linear_mfma_split_kernel<BITS, 5>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
+    }
+    const int64_t MN = (int64_t)M * N;
+    launch(splitk_reduce_kernel, dim3((unsigned)((MN + 1023) / 1024)), dim3(256), 0, stream, e2,
+           (const float*)workspace, y, sp.S, MN);
     return hipGetLastError();
   }
   const int TW = tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1);
@@ -651,8 +751,10 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
 template hipError_t launch_linear_mfma_group<3>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_mfma_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_mfma<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
-                                          uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
+                                          uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&, float*,
+                                          size_t);
 template hipError_t launch_linear_mfma<4>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
-                                          uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
+                                          uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&, float*,
+                                          size_t);
 
 }  // namespace laq

@@ -24,7 +24,8 @@ MAX_GROUP = 8
 
 EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profile_next_launch",
            "laq_quantize_w3g128", "laq_pack_w3g128", "laq_linear_w3g128", "laq_linear_group_w3g128",
-           "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128", "laq_linear_group_w4g128")
+           "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128", "laq_linear_group_w4g128",
+           "laq_linear_workspace_bytes", "laq_linear_ws_w3g128", "laq_linear_ws_w4g128")
 
 
 class LinearCall(ctypes.Structure):
@@ -74,6 +75,12 @@ def lib():
             f = getattr(L, name)
             f.argtypes = [P, P, P, P, P, I64, I64, I64, P]
             f.restype = ctypes.c_int32
+        for name in ("laq_linear_ws_w3g128", "laq_linear_ws_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [P, P, P, P, P, I64, I64, I64, P, I64, P]
+            f.restype = ctypes.c_int32
+        L.laq_linear_workspace_bytes.argtypes = [I64, I64, I64]
+        L.laq_linear_workspace_bytes.restype = I64
         _lib = L
     return _lib
 
@@ -140,8 +147,18 @@ def pack(w, scales, zeros, bits=3, out=None):
     return qweight
 
 
-def linear(x, qweight, scales, zeros, bits=3, out=None):
-    """y = x @ w_hat^T for fp16 x [M][K] (M <= 16) against packed weights."""
+def workspace_bytes(M, N, K):
+    """Workspace with which the linear splits K for this shape (0: never)."""
+    return int(lib().laq_linear_workspace_bytes(M, N, K))
+
+
+def linear(x, qweight, scales, zeros, bits=3, out=None, split_k=True):
+    """y = x @ w_hat^T for fp16 x [M][K] (M <= 16) against packed weights.
+
+    split_k: where the shape gains from splitting K across workgroups
+    (laq_linear_workspace_bytes > 0), take a workspace from torch's allocator
+    on the current stream and call the _ws entry point; False calls the plain
+    entry point."""
     import torch
     assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
     M, K = x.shape
@@ -150,6 +167,13 @@ def linear(x, qweight, scales, zeros, bits=3, out=None):
     assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
     assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
     y = torch.empty((M, N), dtype=torch.float16, device=x.device) if out is None else out
+    nbytes = workspace_bytes(M, N, K) if split_k else 0
+    if nbytes > 0:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device)
+        fn = lib().laq_linear_ws_w3g128 if bits == 3 else lib().laq_linear_ws_w4g128
+        _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _ptr(ws), nbytes,
+                  _stream(x.device)))
+        return y
     fn = lib().laq_linear_w3g128 if bits == 3 else lib().laq_linear_w4g128
     _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _stream(x.device)))
     return y

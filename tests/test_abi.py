@@ -134,6 +134,51 @@ def test_group_validation(L, bits):
     assert b"laq_linear_group" in L.laq_last_error()
 
 
+def _lin_ws(L, bits, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, M=4, N=4, K=128, ws=FAKE, wsb=1024):
+    f = L.laq_linear_ws_w3g128 if bits == 3 else L.laq_linear_ws_w4g128
+    return f(ctypes.c_void_p(x), ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z),
+             ctypes.c_void_p(y), M, N, K, ctypes.c_void_p(ws), wsb, None)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_ws_validation(L, bits):
+    for kw in ("x", "q", "s", "z", "y"):
+        assert _lin_ws(L, bits, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _lin_ws(L, bits, ws=0, wsb=16) == laq.LAQ_ERR_NULL_POINTER
+    assert _lin_ws(L, bits, wsb=-1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lin_ws(L, bits, M=0) == laq.LAQ_ERR_BAD_M
+    assert _lin_ws(L, bits, M=17) == laq.LAQ_ERR_BAD_M
+    assert _lin_ws(L, bits, K=200) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lin_ws(L, bits, x=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert _lin_ws(L, bits, y=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert _lin_ws(L, bits, ws=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_linear_ws" in L.laq_last_error()
+
+
+def test_workspace_bytes(L):
+    """The workspace holds S fp32 partial planes of M x N, one per K range of
+    at most five quads (512-column blocks), when the row has at least 40 quads
+    and fewer than 1024 row tiles (M >= 2); 0 otherwise and for invalid
+    shapes."""
+    f = L.laq_linear_workspace_bytes
+    for (M, N, K) in [(16, 5120, 25600), (3, 100, 25088), (16, 3, 1 << 24), (8, 16368, 25600), (2, 5120, 20480),
+                      (16, 1030, 20480)]:
+        nq = -(-K // 512)
+        b = f(M, N, K)
+        assert b > 0 and b % (M * N * 4) == 0, (M, N, K)
+        S = b // (M * N * 4)
+        assert -(-nq // 5) <= S <= nq, (M, N, K, S)
+        qs = -(-nq // S)  # quads per range
+        assert -(-nq // qs) == S, (M, N, K, S)
+    assert f(16, 5120, 25600) == 10 * 16 * 5120 * 4  # 80 blocks of four tiles x 10 ranges of 5 quads
+    assert f(1, 5120, 25600) == 0         # one row: the VALU GEMV, no split
+    assert f(16, 16384, 25600) == 0       # >= 1024 row tiles: blocks of several tiles
+    assert f(16, 5120, 19968) == 0        # 39 quads
+    assert f(16, 2560, 9728) == 0
+    for (M, N, K) in [(0, 4, 128), (17, 4, 128), (4, 0, 128), (4, 4, 100), (4, 4, 1 << 25), (4, 1 << 31, 128)]:
+        assert f(M, N, K) == 0
+
+
 def test_shape_check_precedes_m_check(L):
     # a bad shape is reported even when M is also bad
     assert _lin(L, 3, M=0, K=100) == laq.LAQ_ERR_BAD_SHAPE

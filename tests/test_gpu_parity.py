@@ -7,6 +7,8 @@ Inputs are seeded (paper_2605_08755_amd.inputs); the linear is fed the
 oracle's own quantization, so its parity does not depend on the quantize
 kernel.
 """
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -423,6 +425,61 @@ def test_matrix_core_walk_ragged():
         assert r["ok"], (M, r)
     del q, sd, zd
     torch.cuda.empty_cache()
+
+
+SPLIT_SHAPES = [(5120, 25600), (100, 25088), (3, 20608), (1030, 20480)]
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("N,K", SPLIT_SHAPES)
+def test_split_k(bits, N, K):
+    """K split across workgroups of four row tiles (rows of >= 40 quads, fewer
+    than 1024 tiles): the Qwen3-32B down projection (ranges of five quads), a
+    partial last quad (K = 25088: 196 groups; K = 20608: 161), a last block
+    with idle tiles (N = 100, 1030) and a single partial tile (N = 3), ranges
+    of one quad; against the oracle, deterministic, and the plain entry point
+    also within tolerance."""
+    say("split K", bits, N, K)
+    assert laq.workspace_bytes(16, N, K) > 0
+    w = inputs.weights(N, K, cfg=19, layer=bits, proj=K % 83)
+    codes, qw, s, z = oracle_packed(w, bits)
+    qd, sd, zd = to_dev(qw.view(np.int32)), to_dev(s.view(np.float16)), to_dev(z)
+    for M in (2, 3, 5, 8, 16):
+        x = inputs.activations(M, K, cfg=19, layer=M)
+        xd = to_dev(x)
+        y1 = laq.linear(xd, qd, sd, zd, bits)
+        y2 = laq.linear(xd, qd, sd, zd, bits)
+        yp = laq.linear(xd, qd, sd, zd, bits, split_k=False)
+        torch.cuda.synchronize()
+        ref = oracle.linear(x, codes, s, z)
+        assert torch.equal(y1, y2), M
+        r = linear_check(y1.cpu().numpy(), ref)
+        assert r["ok"], (M, r)
+        r = linear_check(yp.cpu().numpy(), ref)
+        assert r["ok"], (M, "plain", r)
+
+
+def test_split_k_small_workspace():
+    """A workspace smaller than laq_linear_workspace_bytes: the _ws call is
+    the plain call, bit for bit."""
+    N, K, M = 1030, 20480, 16
+    say("split K small workspace", N, K, M)
+    w = inputs.weights(N, K, cfg=20, layer=1)
+    codes, qw, s, z = oracle_packed(w, 3)
+    qd, sd, zd = to_dev(qw.view(np.int32)), to_dev(s.view(np.float16)), to_dev(z)
+    xd = to_dev(inputs.activations(M, K, cfg=20, layer=2))
+    need = laq.workspace_bytes(M, N, K)
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    y = torch.empty((M, N), dtype=torch.float16, device=DEV)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    st = laq.lib().laq_linear_ws_w3g128(ctypes.c_void_p(xd.data_ptr()), ctypes.c_void_p(qd.data_ptr()),
+                                        ctypes.c_void_p(sd.data_ptr()), ctypes.c_void_p(zd.data_ptr()),
+                                        ctypes.c_void_p(y.data_ptr()), M, N, K, ctypes.c_void_p(ws.data_ptr()),
+                                        need - 16, stream)
+    assert st == laq.LAQ_OK
+    yp = laq.linear(xd, qd, sd, zd, 3, split_k=False)
+    torch.cuda.synchronize()
+    assert torch.equal(y, yp)
 
 
 # ---------------------------------------------------------------------------
