@@ -18,6 +18,7 @@
 // The waves of a block split the groups of the block's 16 rows; their
 // partial sums are added in a fixed order through LDS (deterministic).
 #include <type_traits>
+#include <utility>
 
 #include "laq_internal.h"
 
@@ -105,6 +106,43 @@ __device__ __forceinline__ void unpack_chunk_exact(const uint32_t (&w)[BITS], ui
 __device__ __forceinline__ half8_t frag(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
   typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
   return __builtin_bit_cast(half8_t, u32x4v{a, b, c, d});
+}
+
+// Fragment reads from an LDS slab that direct-to-LDS loads fill, written as
+// inline assembly on purpose: the compiler's wait insertion treats any LDS
+// read that follows a direct-to-LDS load as dependent on every such load in
+// flight, so it would wait for the loads of later quads too.  The waits the
+// data flow needs are explicit instead: vmcnt before the barrier that
+// publishes a slab, lgkmcnt (lds_wait) before the fragments are used.
+__device__ __forceinline__ uint32_t lds_addr(const u32x4* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) u32x4*)p;
+}
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+// Waits for the outstanding LDS reads; the fragments pass through the
+// statement, so no use of them is scheduled before the wait.
+__device__ __forceinline__ void lds_wait(u32x4 (&f)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]));
+}
+
+// s_waitcnt vmcnt(N) (other counters unconstrained), N a compile-time constant <= 63.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | (((N >> 4) & 3) << 14));
+}
+
+// f(std::integral_constant<int, I>{}) for I = 0 .. N-1, in order.
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 // An offset past every buffer extent: the load returns zero and moves no data.
@@ -447,6 +485,7 @@ __global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
 // only feed result rows that are not stored.
 // ---------------------------------------------------------------------------
 constexpr int kFullTiles = 4;
+constexpr int kFullAhead = 1;  // quads requested ahead of the one computed (1 measured best; 2, 3 slower)
 
 // Quads q0 .. q0+NQ-1 (those past the row read zeros).  part == nullptr: the
 // result goes to y as fp16; otherwise the fp32 partial sums go to
@@ -471,28 +510,46 @@ __device__ __forceinline__ void mfma_full_block(
   const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
   const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
 
-  // 1. Every load of the block: slab rows wave, wave + 4, ... (< M) of each
-  //    quad, then the wave's weights of each quad.  Columns past K and groups
-  //    past G read zeros.
+  // 1. Loads, quad by quad: the wave's four slab rows (wave, wave + 4,
+  //    wave + 8, wave + 12; rows >= M, columns past K and groups past G read
+  //    zeros), then its weights of the quad: XL + WL loads per quad, issued in
+  //    this order (scheduling barriers), so that a wait for quad q can leave
+  //    the later quads' loads in flight.  Quads are requested kFullAhead ahead
+  //    of the one computed: a wave that requested everything first would sit
+  //    in the issue of its last loads (the vector-memory pipe is the slow
+  //    part) before it could start computing.
+  constexpr int XL = 16 / kFullTiles;
+  constexpr int WL = BITS + 2;
+  constexpr int D = NQ < kFullAhead ? NQ : kFullAhead;
+  static_assert(D * (XL + WL) <= 63, "outstanding loads exceed the vmcnt range");
+  QuadWeights<BITS> wq[NQ];
+  auto issue = [&](auto qc) {
+    constexpr int q = decltype(qc)::value;
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    for (int m = wave; m < M; m += kFullTiles) {
+    for (int i = 0; i < XL; ++i) {
+      const int m = wave + i * kFullTiles;
       const int col = 512 * (q0 + q) + 8 * (lane ^ (m & 7));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(slab + (q * 16 + m) * 64), 16,
-                                               col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
+                                               m < M && col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0,
+                                               0, 0);
     }
-  }
-  QuadWeights<BITS> wq[NQ];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) wq[q] = load_quad<BITS, kWeightPolicyNT>(qr, sr, zr, nl, j, q0 + q, G, true);
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
-  __syncthreads();
+    wq[q] = load_quad<BITS, kWeightPolicyNT>(qr, sr, zr, nl, j, q0 + q, G, true);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  static_for<D>(issue);
 
-  // 2. The tile's quads.
+  // 2. Quad by quad: wait until only the later quads' loads are outstanding,
+  //    a bare barrier (the other waves' slab rows; a __syncthreads() fence
+  //    would wait for every load in flight), request quad q + D, compute.
   float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
   const int swz = nl & 7;
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
+  static_for<NQ>([&](auto qc) {
+    constexpr int q = decltype(qc)::value;
+    constexpr int issued = q + D < NQ ? q + D : NQ;  // quads requested so far
+    wait_vmcnt<(issued - q - 1) * (XL + WL)>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (q + D < NQ) issue(std::integral_constant<int, q + D>{});
     // Quarter transposes: chunk j of group 4q + gi in component gi.
     uint32_t wt[BITS][4];
 #pragma unroll
@@ -507,25 +564,28 @@ __device__ __forceinline__ void mfma_full_block(
     szj[0] = szj[1] = szj[2] = szj[3] = wq[q].s | (wq[q].z << 16);
     transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
 
-    const u32x4* sl = slab + (q * 16 + nl) * 64;
+    const uint32_t sa = lds_addr(slab + (q * 16 + nl) * 64);
 #pragma unroll
     for (int gi = 0; gi < 4; ++gi) {
+      u32x4 fr[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) fr[jj] = lds_read_b128(sa + 16 * ((16 * gi + 4 * j + jj) ^ swz));
       uint32_t w[BITS];
 #pragma unroll
       for (int p = 0; p < BITS; ++p) w[p] = wt[p][gi];
       uint32_t pr[16];
       unpack_chunk_exact<BITS>(w, szj[gi] >> 16, pr);
+      lds_wait(fr);
       float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const half8_t a = __builtin_bit_cast(half8_t, sl[(16 * gi + 4 * j + jj) ^ swz]);
         const half8_t b = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
-        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, fr[jj]), b, c, 0, 0, 0);
       }
       const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[gi] & 0xFFFFu));
       yacc += s * c;
     }
-  }
+  });
 
   // 3. Lane (n, j) holds rows m = 4j .. 4j+3 of column n.
 #pragma unroll
