@@ -15,8 +15,13 @@
 // 2^(10-p) + q exactly; one packed fp16 add of -(2^(10-p) + z) leaves q - z
 // exactly.  One v_and_or_b32 + one v_pk_add_f16 per two codes.
 //
-// The waves of a block split the groups of the block's 16 rows; their
-// partial sums are added in a fixed order through LDS (deterministic).
+// Kernels: one or two 16-row tiles per block, its waves splitting the row's
+// quads, partial sums added in a fixed order through LDS (fewer than 1024
+// tiles); four tiles per block sharing each activation slab, requesting one
+// quad ahead (many tiles, K <= 2560; also the K ranges of split K, whose fp32
+// partials a second kernel adds in order); four or eight tiles per block
+// walking K one quad at a time (many tiles, longer rows).  Every reduction
+// order is fixed, so results are deterministic.
 #include <type_traits>
 #include <utility>
 
@@ -308,7 +313,8 @@ __device__ __forceinline__ void mfma_block(
 }
 
 // ---------------------------------------------------------------------------
-// Activation-sharing variant for many row tiles.  A block of TB waves owns TB
+// Activation-sharing variant for many row tiles and rows longer than five
+// quads (K > 2560).  A block of TB waves owns TB
 // consecutive 16-row tiles, one per wave, and walks K one quad (4 groups =
 // 512 columns) at a time.  The quad's activation slab x[0..15][512q ..
 // 512q+511] (rows past M read as zero) goes straight from memory into LDS
@@ -473,16 +479,15 @@ __global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Rows of at most five quads (K <= 2560) with many row tiles: one memory
-// round trip per wave.  A block of four waves owns four 16-row tiles, one per
-// wave, and requests everything at once: the activation slabs of all NQ quads
-// (each slab once per block, x[0..M-1][512q .. 512q+511] into LDS by
-// direct-to-LDS loads, four rows per wave) and the wave's weights of all NQ
-// quads (registers).  After one wait and one barrier the wave computes its
-// tile's NQ quads.  The walk-one-quad-at-a-time kernel above pays one round
-// trip per quad instead (its prefetch is one quad ahead, and a quad's compute
-// is far shorter than a round trip).  Slab rows m >= M are not written and
-// only feed result rows that are not stored.
+// Rows of at most five quads (K <= 2560) with many row tiles, and the K
+// ranges of split K.  A block of four waves owns four 16-row tiles, one per
+// wave, and keeps the activation slabs of all its NQ quads (each slab once
+// per block, x[0..M-1][512q .. 512q+511] into LDS by direct-to-LDS loads, four
+// rows per wave; rows past M read zeros) and the wave's weights of all NQ
+// quads (registers).  Quad q + 1 is requested before quad q is computed, so
+// its loads land during that compute; requesting everything first kept each
+// wave in the issue of its last loads, with nothing to compute, for most of
+// the time the data took to arrive.
 // ---------------------------------------------------------------------------
 constexpr int kFullTiles = 4;
 constexpr int kFullAhead = 1;  // quads requested ahead of the one computed (1 measured best; 2, 3 slower)
