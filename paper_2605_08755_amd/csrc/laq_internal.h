@@ -51,6 +51,8 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
 // internally so measurement harnesses can sweep them).
 struct LinearTuning {
   int flat_threads = 0;      // flat kernel: threads per block (64 .. 1024); 0 = chosen from the shape
+  int flat_rpl = 0;          // flat kernel: rows per lane (1 or 2); 0 = chosen from the shape
+  int flat_resident_waves = 8192;  // waves the chip keeps resident (256 compute units x 32)
   int last_blocks = 0;       // launch shape of the most recent flat launch (for harnesses)
   int last_rows = 0;
   int mfma_min_m = 3;        // activation rows from which the matrix-core path may be used

@@ -266,6 +266,43 @@ __device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[XB], int base, in
   }
 }
 
+// Dot products of RPL units that share group g (rows of one lane): the
+// group's activations are read from LDS once per chunk and used for every
+// row, so LDS reads per weight fall by RPL.
+template <int BITS, int MT, int RPL>
+__device__ __forceinline__ void units_dot(const u32x4 (&wv)[RPL][BITS], const u32x4* xl, int G, int g,
+                                          float (&acc)[RPL][MT][4]) {
+#pragma unroll
+  for (int i = 0; i < RPL; ++i)
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[i][m][c] = 0.0f;
+#pragma unroll
+  for (int cc = 0; cc < 4; ++cc) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const u32x4* xp4 = xl + (m * G + g) * kGroupStrideU4 + cc * 4;
+      uint32_t xp[16];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const u32x4 q = xp4[v];
+        xp[4 * v + 0] = q.x;
+        xp[4 * v + 1] = q.y;
+        xp[4 * v + 2] = q.z;
+        xp[4 * v + 3] = q.w;
+      }
+#pragma unroll
+      for (int i = 0; i < RPL; ++i) {
+        uint32_t w[BITS];
+#pragma unroll
+        for (int p = 0; p < BITS; ++p) w[p] = wv[i][p][cc];
+        chunk_dot<BITS>(w, xp, acc[i][m]);
+      }
+    }
+  }
+}
+
 // One block of the flat kernel: rows block*R .. block*R + R - 1 of one call.
 template <int BITS, int MT, int NT, int UPT, int XB>
 __device__ __forceinline__ void flat_block(
@@ -410,7 +447,97 @@ __device__ __forceinline__ void flat_block(
   }
 }
 
-template <int BITS, int MT, int NT, int UPT, int XB>
+// One block of the flat kernel with RPL rows per lane: the block's R rows
+// form RPL layers of R1 = R / RPL rows (R1 * G <= NT), and thread
+// t = r*G + g of the first layer takes group g of rows r, r + R1, r + 2*R1,
+// ...  Loads, staging and the row sums are those of flat_block.
+template <int BITS, int MT, int NT, int RPL, int XB>
+__device__ __forceinline__ void flat_block_rpl(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
+    int block) {
+  extern __shared__ u32x4 lds[];
+  u32x4* xl = lds;                                                                // [MT][G][17]
+  float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
+  float* part = xsum + MT * G;                                                    // [MT][R*G]
+
+  const int t = threadIdx.x;
+  // An idle block (an XCD-rounding slot past the last row) has rows = 0: every
+  // buffer extent is zero, so it loads and stores nothing.
+  const int64_t row0 = (int64_t)block * R;
+  const int rows = (int)max((int64_t)0, min((int64_t)R, (int64_t)N - row0));
+  const int U = rows * G;
+  const int XU = MT * G * 16;  // activation tile in 16-byte units (rows m >= M read as zero)
+  const int R1 = R / RPL;
+
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, (uint32_t)M * G * 256);
+  const __amdgpu_buffer_rsrc_t qr = make_rsrc(qw + row0 * BITS * G * 4, (uint32_t)rows * BITS * G * 16);
+  const __amdgpu_buffer_rsrc_t sr = make_rsrc(scales + row0 * G, (uint32_t)U * 2);
+  const __amdgpu_buffer_rsrc_t zr = make_rsrc(zeros + row0 * G, (uint32_t)U);
+
+  // Thread t = r0*G + g0 (t / G computed as in flat_block).  Threads past
+  // the first layer (r0 >= R1) own no unit: their loads start at row R,
+  // past every extent, and read zeros.
+  const int r0 = (int)(((float)t + 0.5f) * inv_g);
+  const int g0 = t - r0 * G;
+  const int rb = r0 < R1 ? r0 : R;
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 1. First pass of activation loads (needed first: they are staged while
+  //    the weights stream in), then at once the weights of this thread's
+  //    units.  The scheduling barrier keeps the activation processing below
+  //    from being hoisted between the two batches of loads, which would make
+  //    the weight stream wait for an activation round trip.
+  //    Index XM = M*G*16 is the end of x's extent: loads past it read zero.
+  u32x4 xv[XB];
+#pragma unroll
+  for (int i = 0; i < XB; ++i)
+    xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
+  u32x4 wv[RPL][BITS];
+  float sv[RPL], zv[RPL];
+#pragma unroll
+  for (int i = 0; i < RPL; ++i) load_flat_unit<BITS>(qr, sr, zr, rb + i * R1, g0, G, wv[i], sv[i], zv[i]);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 2. Stage activations and per-group sums (first pass from the loads above).
+  stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);
+  for (int base = XB * NT; base < XU; base += XB * NT) {
+#pragma unroll
+    for (int i = 0; i < XB; ++i)
+      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(base + t + i * NT) * 16, 0, 0);
+    stage_x_pass<MT, NT, XB>(xv, base, t, XU, xl, xsum);
+  }
+  __syncthreads();
+
+  // 3. Units: the partial of unit (r, g) goes to part[m][r*G + g].
+  // Rows past `rows` read zero weights, scales and zero points, so their
+  // partials are zero (and never summed).
+  if (r0 < R1) {
+    float acc[RPL][MT][4];
+    units_dot<BITS, MT, RPL>(wv, xl, G, g0, acc);
+#pragma unroll
+    for (int i = 0; i < RPL; ++i)
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+        part[m * R * G + (r0 + i * R1) * G + g0] =
+            sv[i] * fmaf(-zv[i], xsum[m * G + g0], classes_to_value<BITS>(acc[i][m]));
+  }
+  __syncthreads();
+
+  // 4. Row sums in a fixed order: lane l of a row's 16 adds groups l, l+16, ...
+  const int l = t & 15;
+  for (int rr = t >> 4; rr < rows; rr += NT / 16) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float acc = 0.0f;
+      for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
+      acc = row16_sum(acc);
+      if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+    }
+  }
+}
+
+template <int BITS, int MT, int NT, int RPL, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
@@ -418,14 +545,17 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
   // Slots of the XCD-rounded grid past nblocks get rows = 0 in flat_block (no
   // early return: the argument loads then go out as one batch).
   (void)nblocks;
-  flat_block<BITS, MT, NT, UPT, XB>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+  if constexpr (RPL == 1)
+    flat_block<BITS, MT, NT, 1, XB>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+  else
+    flat_block_rpl<BITS, MT, NT, RPL, XB>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
 }
 
 // Several independent calls in one launch: block b belongs to the last call
 // whose first block is <= b.  The call's fields are picked with constant
 // indices (uniform selects), so the argument block is never indexed at run
 // time.
-template <int BITS, int MT, int NT, int UPT, int XB>
+template <int BITS, int MT, int NT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup grp, int M) {
   // Slots past the last call's blocks fall to that call with rows = 0.
   const int b = xcd_block();
@@ -433,7 +563,7 @@ __global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup
 #pragma unroll
   for (int j = 1; j < kMaxGroup; ++j)
     if (j < grp.count && b >= grp.call[j].first_block) c = grp.call[j];
-  flat_block<BITS, MT, NT, UPT, XB>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, c.R, c.inv_g, b - c.first_block);
+  flat_block<BITS, MT, NT, 1, XB>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, c.R, c.inv_g, b - c.first_block);
 }
 
 int ceil_pow2(int v) {
@@ -473,29 +603,64 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     // longer rows want more rows per block (about 8 or more) to amortize it;
     // short rows with few of them use smaller blocks so that the grid still
     // covers the compute units.
-    int NT = tune.flat_threads > 0 ? tune.flat_threads : (G <= 32 ? 256 : (G <= 64 ? 512 : 1024));
+    // Rows of 65..128 groups use 256 threads at one activation row and 512
+    // at two, with two rows per lane (below).
+    int NT = tune.flat_threads;
+    if (NT == 0) NT = G <= 32 ? 256 : G <= 64 ? 512 : G <= 128 ? (MT == 1 ? 256 : 512) : 1024;
     if (tune.flat_threads == 0 && MT == 1)
       while (NT > 64 && G <= 16 && NT / 2 >= G && (N + NT / G - 1) / (NT / G) < 256) NT /= 2;
     const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
+    auto lds_bytes = [&](int rows) { return (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * rows * G * 4; };
     int R = max(1, NT / G);
     R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
-    const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
+    // Rows per lane: a thread takes group g of RPL rows, so every activation
+    // group read from LDS serves RPL rows and each block's activation tile
+    // serves RPL times as many rows; the lane's dot products get RPL times
+    // longer.  Measured on MI355X, two rows per lane pay off when
+    //  - one activation row has 65..128 groups,
+    //  - the grid at one row per lane holds more waves than the chip keeps
+    //    resident (32 per compute unit), so waves would run in several rounds,
+    //  - two activation rows meet rows of 32..128 groups (twice the LDS
+    //    reads per unit);
+    // elsewhere one row per lane is faster (the lanes' own latency decides).
+    int want = tune.flat_rpl;
+    if (want == 0) {
+      const int64_t waves1 = (N + R - 1) / R * (NT / 64);
+      if (MT == 1)
+        want = (G > 64 && G <= 128) || (G <= 64 && waves1 > tune.flat_resident_waves) ? 2 : 1;
+      else
+        want = (MT == 2 && G >= 32 && G <= 128) ? 2 : 1;
+    }
+    int RPL = 1;
+    if (want > 1 && NT >= 256 && G <= NT) {
+      const int r1 = min(NT / G, 4096 / (G * MT * want));
+      if (r1 >= 1 && lds_bytes(want * r1) <= 64 * 1024) {
+        RPL = want;
+        R = want * r1;
+      }
+    }
+    const size_t lds = lds_bytes(R);
     if (MT <= 4 && lds <= 64 * 1024) {
       const int nblocks = (int)((N + R - 1) / R);
       const unsigned blocks = xcd_grid(nblocks);
       tune.last_blocks = nblocks;
       tune.last_rows = R;
-#define LAQ_FLAT_NT(MTV, XBV, NTV)                                                                          \
-  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
+#define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                        \
+  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
          qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+#define LAQ_FLAT_NT(MTV, XBV, NTV)                       \
+  do {                                                   \
+    if (RPL == 2) LAQ_FLAT_K(MTV, XBV, NTV, 2);          \
+    else LAQ_FLAT_K(MTV, XBV, NTV, 1);                   \
+  } while (0)
 #define LAQ_FLAT(MTV, XBV)                              \
   do {                                                  \
     if (NT == 1024) LAQ_FLAT_NT(MTV, XBV, 1024);        \
     else if (NT == 512) LAQ_FLAT_NT(MTV, XBV, 512);     \
     else if constexpr (MTV > 1) LAQ_FLAT_NT(MTV, XBV, 256); \
     else if (NT == 256) LAQ_FLAT_NT(MTV, XBV, 256);     \
-    else if (NT == 128) LAQ_FLAT_NT(MTV, XBV, 128);     \
-    else LAQ_FLAT_NT(MTV, XBV, 64);                     \
+    else if (NT == 128) LAQ_FLAT_K(MTV, XBV, 128, 1);   \
+    else LAQ_FLAT_K(MTV, XBV, 64, 1);                   \
   } while (0)
 #define LAQ_FLAT_XB(MTV)          \
   if (XB == 2) LAQ_FLAT(MTV, 2);  \
@@ -508,6 +673,7 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
 #undef LAQ_FLAT_XB
 #undef LAQ_FLAT
 #undef LAQ_FLAT_NT
+#undef LAQ_FLAT_K
       return hipGetLastError();
     }
   }
@@ -582,7 +748,7 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
     return hipSuccess;
   }
 #define LAQ_FLAT_G(MTV, XBV, NTV)                                                                         \
-  launch(linear_flat_group_kernel<BITS, MTV, NTV, 1, XBV>, dim3(xcd_grid(blocks)), dim3(NTV), (uint32_t)lds, \
+  launch(linear_flat_group_kernel<BITS, MTV, NTV, XBV>, dim3(xcd_grid(blocks)), dim3(NTV), (uint32_t)lds, \
          stream, ev, grp, M)
 #define LAQ_FLAT_GN(MTV, XBV)                              \
   do {                                                     \

@@ -186,7 +186,7 @@ def test_pack_canary():
 # ---------------------------------------------------------------------------
 # linear
 # ---------------------------------------------------------------------------
-LSHAPES = [(1, 128), (17, 384), (64, 128), (300, 2560), (1024, 1024), (4096, 1024), (257, 4096), (96, 9728), (3, 25600)]
+LSHAPES = [(1, 128), (17, 384), (64, 128), (300, 2560), (1024, 1024), (4096, 1024), (257, 4096), (100, 9728), (3, 25600)]
 
 
 @pytest.mark.parametrize("bits", [3, 4])
