@@ -150,8 +150,9 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// An offset past every buffer extent: the load returns zero and moves no data.
-constexpr uint32_t kOffsetNone = 0x80000000u;
+// Loads of dead lanes (rows past M, columns past K, groups past G) OR bit
+// 31 into their offsets: that is past every buffer extent, so the load
+// returns zero and moves no data.
 
 // 4 x 4 transpose across the four 16-lane quarters of a wave: on entry
 // register c of quarter j holds element (j, c); on exit register j of
@@ -241,7 +242,7 @@ __device__ __forceinline__ void mfma_block(
     for (int m = 0; m < M; ++m) {
       const int col = 512 * Q + 8 * (lane ^ (m & 7));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sl + m * 64), 16,
-                                               col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
+                                               (uint32_t)(m * K + col) * 2 | (uint32_t)!(col < K) << 31, 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): weights and slab
@@ -355,13 +356,14 @@ __device__ __forceinline__ QuadWeights<BITS> load_quad(__amdgpu_buffer_rsrc_t qr
   QuadWeights<BITS> r;
   const int C = 4 * G;
   const int gq = 4 * q + j;
-  const bool ok = live && gq < G;
+  // A dead lane's offsets get bit 31 (past every extent) by an OR: a select
+  // between offsets was compiled into branches that wait at their join.
+  const uint32_t dead = (uint32_t)!(live && gq < G) << 31;
 #pragma unroll
   for (int p = 0; p < BITS; ++p)
-    r.w[p] = __builtin_amdgcn_raw_buffer_load_b128(qr, ok ? (uint32_t)(((n * BITS + p) * C + 4 * gq) * 4) : kOffsetNone,
-                                                   0, AUX);
-  r.s = __builtin_amdgcn_raw_buffer_load_b16(sr, ok ? (uint32_t)(n * G + gq) * 2 : kOffsetNone, 0, 0);
-  r.z = __builtin_amdgcn_raw_buffer_load_b8(zr, ok ? (uint32_t)(n * G + gq) : kOffsetNone, 0, 0);
+    r.w[p] = __builtin_amdgcn_raw_buffer_load_b128(qr, (uint32_t)(((n * BITS + p) * C + 4 * gq) * 4) | dead, 0, AUX);
+  r.s = __builtin_amdgcn_raw_buffer_load_b16(sr, (uint32_t)(n * G + gq) * 2 | dead, 0, 0);
+  r.z = __builtin_amdgcn_raw_buffer_load_b8(zr, (uint32_t)(n * G + gq) | dead, 0, 0);
   return r;
 }
 
@@ -396,28 +398,15 @@ __device__ __forceinline__ void mfma_tiles_block(
       const int m = wave + i * TB;
       const int piece = lane ^ (m & 7);
       const int col = 512 * qq + 8 * piece;
-      const bool ok = m < M && qq < nq && col < K;
+      const uint32_t dead = (uint32_t)!(m < M && qq < nq && col < K) << 31;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(slab + (buf * 16 + m) * 64), 16,
-                                               ok ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0, 0, 0);
+                                               (uint32_t)(m * K + col) * 2 | dead, 0, 0, 0);
     }
   };
 
-  // Issue order X0, W0, X1: waiting until only X1 is outstanding completes
-  // X0 (this wave's part of the slab) and W0.
-  fetch_slab(0);
-  QuadWeights<BITS> cur = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, 0, G, true);
-  fetch_slab(1);
-  __builtin_amdgcn_s_waitcnt(0x0F70 | (XL & 15) | (((XL >> 4) & 3) << 14));
-  __syncthreads();
-
   float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
-  for (int q = 0; q < nq; ++q) {
-    // Quad q + 2's slab, then quad q + 1's weights (loads past the last quad
-    // read zeros; the slab buffer written here was last read in quad q - 1).
-    fetch_slab(q + 2);
-    QuadWeights<BITS> nxt = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, q + 1, G, q + 1 < nq);
-    __builtin_amdgcn_sched_barrier(0);
-
+  // Quad q's products from its weights and slab buffer q % 3.
+  auto compute = [&](const QuadWeights<BITS>& cur, int q) {
     // Quarter transposes: chunk j of group 4q + gi in component gi.
     uint32_t wt[BITS][4];
 #pragma unroll
@@ -451,14 +440,53 @@ __device__ __forceinline__ void mfma_tiles_block(
       const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[gi] & 0xFFFFu));
       yacc += s * c;
     }
-
-    // Quad q + 1's slab (requested one quad ago, before the weights of this
-    // quad's successor) is complete when at most this quad's XL + WL loads
-    // are outstanding; then the barrier publishes it to every wave.
+  };
+  // One quad of the walk: request quad q + 2's slab and weights (into the
+  // register set quad q - 1 used; loads past the last quad read zeros, and
+  // the slab buffer written was last read in quad q - 1), compute quad q,
+  // then wait until only quad q + 2's loads are outstanding, which completes
+  // quad q + 1's, and publish its slab with the barrier.
+  auto step = [&](int q, const QuadWeights<BITS>& cur, QuadWeights<BITS>& ahead) {
+    fetch_slab(q + 2);
+    ahead = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, q + 2, G, q + 2 < nq);
     __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_waitcnt(0x0F70 | ((XL + WL) & 15) | ((((XL + WL) >> 4) & 3) << 14));
-    __syncthreads();
-    cur = nxt;
+    compute(cur, q);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<XL + WL>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Three register sets of quad weights in turn, so that no load waits for
+  // a register copy: the loop is unrolled by three.  Issue order X0, W0,
+  // X1, W1: waiting until only X1 and W1 are outstanding completes X0 (this
+  // wave's part of the slab) and W0.
+  QuadWeights<BITS> wa, wb, wc;
+  fetch_slab(0);
+  wa = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, 0, G, true);
+  __builtin_amdgcn_sched_barrier(0);
+  fetch_slab(1);
+  wb = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, 1, G, 1 < nq);
+  __builtin_amdgcn_sched_barrier(0);
+  wait_vmcnt<XL + WL>();
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  int q = 0;
+  for (; q + 3 <= nq; q += 3) {
+    step(q, wa, wc);
+    step(q + 1, wb, wa);
+    step(q + 2, wc, wb);
+  }
+  // The last one or two quads: their loads are in flight already.
+  if (q < nq) {
+    compute(wa, q);
+    if (q + 1 < nq) {
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      compute(wb, q + 1);
+    }
   }
 
   // Lane (n, j) holds rows m = 4j .. 4j+3 of column n.
@@ -535,8 +563,8 @@ __device__ __forceinline__ void mfma_full_block(
       const int m = wave + i * kFullTiles;
       const int col = 512 * (q0 + q) + 8 * (lane ^ (m & 7));
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(slab + (q * 16 + m) * 64), 16,
-                                               m < M && col < K ? (uint32_t)(m * K + col) * 2 : kOffsetNone, 0,
-                                               0, 0);
+                                               (uint32_t)(m * K + col) * 2 | (uint32_t)!(m < M && col < K) << 31,
+                                               0, 0, 0);
     }
     wq[q] = load_quad<BITS, kWeightPolicyNT>(qr, sr, zr, nl, j, q0 + q, G, true);
     __builtin_amdgcn_sched_barrier(0);
