@@ -176,22 +176,24 @@ __device__ __forceinline__ void transpose_quarters(uint32_t& r0, uint32_t& r1, u
 // load per plane of row n, group 4Q + j (four chunks), so each row of a tile
 // reads 64 contiguous bytes per plane, and the scale and zero point of that
 // (row, group).  The quad's activations x[0..M-1][512Q .. 512Q+511] go into
-// the wave's own LDS slab with 16-byte direct-to-LDS loads, one fully
-// coalesced 1 KiB row piece per instruction (fragment loads straight from
-// memory would touch 64 separate cache lines per instruction); slab rows m >=
-// M are not written and only feed result rows that are not stored.  A
+// the wave's own LDS slab of M rows with 16-byte direct-to-LDS loads, one
+// fully coalesced 1 KiB row piece per instruction (fragment loads straight
+// from memory would touch 64 separate cache lines per instruction); lanes of
+// activation rows m >= M read row M - 1, which feeds only result rows that
+// are not stored.  A slab of M rows (not 16) lets small M keep more waves
+// resident.  A
 // quarter transpose then gives quarter q chunk q of every group of the quad,
 // the layout the matrix core wants (lane (n, q) supplies row n's codes 32q ..
 // 32q+31 of the group).  Slots past the last group read zeros.
-constexpr int kWaveSlabU4 = 16 * 64;  // one wave's slab: 16 rows x 64 pieces of 16 bytes
-constexpr int kMaxSlabWaves = 10;     // 160 KiB of LDS per block
+constexpr int kSlabRowU4 = 64;          // one slab row: 64 pieces of 16 bytes
+constexpr int kBlockLdsU4 = 160 * 64;   // 160 KiB of LDS per block
 
 template <int BITS, int TW>
 __device__ __forceinline__ void mfma_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
   typedef __attribute__((address_space(3))) void lds_void;
-  extern __shared__ u32x4 wslabs[];  // [W][16 rows][64 pieces]; afterwards the wave's partials
+  extern __shared__ u32x4 wslabs[];  // [W][M rows][64 pieces]; afterwards the wave's partials
 
   const int K = 128 * G;
   const int W = (int)(blockDim.x >> 6);
@@ -203,8 +205,9 @@ __device__ __forceinline__ void mfma_block(
   const int rows = (int)min((int64_t)16 * TW, (int64_t)N - row0);
   const int C = 4 * G;
   const int nq = (G + 3) >> 2;
-  u32x4* const sl = wslabs + wave * kWaveSlabU4;
+  u32x4* const sl = wslabs + wave * (M * kSlabRowU4);
   const int swz = nl & 7;
+  const int arow = min(nl, M - 1);  // activation row read by this lane
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
   const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * C, (uint32_t)rows * BITS * C * 4);
@@ -272,7 +275,7 @@ __device__ __forceinline__ void mfma_block(
     for (int j = 0; j < 4; ++j) {
       half8_t a[4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) a[jj] = __builtin_bit_cast(half8_t, sl[nl * 64 + ((16 * j + 4 * q + jj) ^ swz)]);
+      for (int jj = 0; jj < 4; ++jj) a[jj] = __builtin_bit_cast(half8_t, sl[arow * 64 + ((16 * j + 4 * q + jj) ^ swz)]);
 #pragma unroll
       for (int t = 0; t < TW; ++t) {
         uint32_t w[BITS];
@@ -292,10 +295,11 @@ __device__ __forceinline__ void mfma_block(
     }
   }
 
-  // 4. Fixed-order reduction of the W waves' partials (each wave's partials
-  //    go into its own slab, whose reads have all returned).
+  // 4. Fixed-order reduction of the W waves' partials (each wave's partials,
+  //    TW KiB, go into its own slab of M >= TW KiB, whose reads have all
+  //    returned).
   float* red = reinterpret_cast<float*>(wslabs);
-  constexpr int kWaveSlabF = kWaveSlabU4 * 4;
+  const int kWaveSlabF = M * kSlabRowU4 * 4;
 #pragma unroll
   for (int t = 0; t < TW; ++t)
 #pragma unroll
@@ -800,16 +804,18 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
            (const float*)workspace, y, sp.S, MN);
     return hipGetLastError();
   }
-  const int TW = tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1);
-  // One wave per quad of the row, at most 16 / TW (register budget) and
-  // kMaxSlabWaves (a 16 KiB activation slab per wave); longer rows loop.
-  const int wmax = min(16 / TW, kMaxSlabWaves);
+  // (At most M tiles per wave: a wave's TW KiB of partials reuse its M KiB slab.)
+  const int TW = min(M, tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1));
+  // One wave per quad of the row, at most 16 / TW (register budget) and as
+  // many M-row activation slabs (M KiB each) as fit in 160 KiB; longer rows
+  // loop.
+  const int wmax = min(16 / TW, kBlockLdsU4 / (M * kSlabRowU4));
   const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
   const int nblocks = (int)((tiles + TW - 1) / TW);
   const unsigned blocks = xcd_grid(nblocks);
   tune.last_blocks = nblocks;
   tune.last_rows = 16 * TW;
-  const uint32_t lds = (uint32_t)W * kWaveSlabU4 * 16;
+  const uint32_t lds = (uint32_t)W * M * kSlabRowU4 * 16;
   if (TW == 2)
     launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,
            (int)N, G, nblocks);
@@ -835,9 +841,9 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
   }
   grp.count = count;
   grp.blocks = (int)blocks;
-  const int W = min(kMaxSlabWaves, nq_max);
-  launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * kWaveSlabU4 * 16, stream,
-         ev, grp, M);
+  const int W = min(min(16, kBlockLdsU4 / (M * kSlabRowU4)), nq_max);
+  launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * M * kSlabRowU4 * 16,
+         stream, ev, grp, M);
   return hipGetLastError();
 }
 

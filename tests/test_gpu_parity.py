@@ -401,6 +401,48 @@ def test_matrix_core_shared_slab(bits, N, K):
         assert r["ok"], (M, r)
 
 
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("K", [3072, 4096])
+def test_matrix_core_walk_four_tiles(bits, K):
+    """1024..3071 row tiles walk K in blocks of four tiles, the quad weights
+    in three register sets in turn: K = 3072 (6 quads, the unrolled loop
+    ends exactly) and 4096 (8 quads, two quads after the loop); N = 16400 =
+    1025 * 16 (a last block with one tile).  Sampled rows and the last rows."""
+    N = 16400
+    say("mfma walk four tiles", bits, N, K)
+    rng = np.random.default_rng(K + bits)
+    w = inputs.weights(N, K, cfg=19, layer=bits, proj=K % 97)
+    rows = np.concatenate([np.sort(rng.choice(N - 16, 48, replace=False)), np.arange(N - 16, N)])
+    codes, qw, s, z = oracle_packed(np.ascontiguousarray(w[rows]), bits)
+    wd = to_dev(w)
+    q, sd, zd = laq.quantize(wd, bits)
+    del wd
+    torch.cuda.synchronize()
+    assert np.array_equal(q[rows].cpu().numpy().view(np.uint32), qw)
+    for M in (3, 16):
+        x = inputs.activations(M, K, cfg=19, layer=M)
+        y = laq.linear(to_dev(x), q, sd, zd, bits)
+        torch.cuda.synchronize()
+        r = linear_check(y.cpu().numpy()[:, rows], oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
+    del q, sd, zd
+
+
+@pytest.mark.parametrize("M", [3, 5])
+def test_matrix_core_two_tiles_per_wave_small_m(M):
+    """Fewer than 1024 tiles, at least 256 of them and rows of 32 groups or
+    more: each wave takes two tiles, and its two KiB of partials reuse an
+    activation slab of only M rows.  N = 4100 (ragged), K = 4096."""
+    N, K = 4100, 4096
+    say("mfma two tiles per wave", M, N, K)
+    w = inputs.weights(N, K, cfg=20, layer=M)
+    x = inputs.activations(M, K, cfg=20, layer=M)
+    codes, qw, s, z = oracle_packed(w, 3)
+    y = gpu_linear(x, qw, s, z, 3)
+    r = linear_check(y, oracle.linear(x, codes, s, z))
+    assert r["ok"], r
+
+
 def test_matrix_core_walk_ragged():
     """From 3072 row tiles, blocks of eight tiles walk K one quad at a time
     (K > 2560): N = 49168 = 3073 * 16 (a last block with one tile), K = 3200
