@@ -304,6 +304,8 @@ __device__ __forceinline__ void units_dot(const u32x4 (&wv)[RPL][BITS], const u3
 }
 
 // One block of the flat kernel: rows block*R .. block*R + R - 1 of one call.
+// Thread t takes units t + i*NT (i < UPT) of each pass over the block's
+// units; every launch uses UPT = 1 (more units per thread measured slower).
 template <int BITS, int MT, int NT, int UPT, int XB>
 __device__ __forceinline__ void flat_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
