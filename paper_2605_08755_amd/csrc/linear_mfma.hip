@@ -20,7 +20,7 @@
 // tiles); four tiles per block sharing each activation slab, requesting one
 // quad ahead (many tiles, K <= 2560; also the K ranges of split K, whose fp32
 // partials a second kernel adds in order); four or eight tiles per block
-// walking K one quad at a time (many tiles, longer rows).  Every reduction
+// walking K one quad at a time, two quads ahead (many tiles, longer rows).  Every reduction
 // order is fixed, so results are deterministic.
 #include <type_traits>
 #include <utility>
@@ -324,11 +324,10 @@ __device__ __forceinline__ void mfma_block(
 // 512 columns) at a time.  The quad's activation slab x[0..15][512q ..
 // 512q+511] (rows past M read as zero) goes straight from memory into LDS
 // (16-byte direct-to-LDS buffer loads, no registers), once per block for its
-// TB tiles, into one of three buffers: the slab of quad q+2 is requested
-// while quad q is computed.  A wave's weights for quad q+1 are requested
-// before quad q is computed; per lane and quad they are the loads of
-// mfma_block (row n, group 4q + j, one 16-byte load per plane).  One barrier
-// per quad.
+// TB tiles, into one of three buffers.  The slab and the wave's weights of
+// quad q+2 are requested while quad q is computed; per lane and quad the
+// weights are the loads of mfma_block (row n, group 4q + j, one 16-byte load
+// per plane), in one of three register sets in turn.  One barrier per quad.
 //
 // Slab rows are 64 pieces of 16 bytes; piece p of row m sits at position
 // p ^ (m & 7), so the A-fragment reads of a wave (16 rows x 4 pieces) spread
