@@ -20,8 +20,8 @@
 // tiles); four tiles per block sharing each activation slab, requesting one
 // quad ahead (many tiles, K <= 2560; also the K ranges of split K, whose fp32
 // partials a second kernel adds in order); four or eight tiles per block
-// walking K one quad at a time, two quads ahead (many tiles, longer rows).  Every reduction
-// order is fixed, so results are deterministic.
+// walking K one quad at a time, two quads ahead (many tiles, longer rows).
+// Every reduction order is fixed, so results are deterministic.
 #include <type_traits>
 #include <utility>
 
