@@ -189,6 +189,29 @@ def time_graph(stack, M, bits, steps, warmup, step_fn=None):
     return ms, wall
 
 
+def time_calls_graph(fn, reps=5):
+    """Capture the launches fn() makes into a HIP graph and time `reps`
+    replays on the current stream: ms per pass, with no host launch gaps."""
+    import torch
+    fn()  # eager warm-up
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        fn()
+    g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del g
+    return ms
+
+
 def time_fp16_graph(stack, M, steps, warmup):
     """The same step with the fp16 weights through torch's dense GEMM
     (hipBLASLt): the unquantized reference for the quantized speed-up."""
@@ -236,14 +259,10 @@ def stack32b_extra(dev, steps):
         gbs = wb / (ms * 1e-3) / 1e9
         out["w3_m%d" % M] = {"us": round(ms * 1e3, 1), "GBps": round(gbs, 1),
                              "pct_of_hbm_peak": round(gbs / HBM_PEAK_GBS * 100, 2)}
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for i, w in enumerate(st.fp16):
-        laq.quantize(w, 3, out=st.q[3][i])
-    e1.record()
-    torch.cuda.synchronize()
-    qms = e0.elapsed_time(e1)
+    def quantize_all():
+        for i, w in enumerate(st.fp16):
+            laq.quantize(w, 3, out=st.q[3][i])
+    qms = time_calls_graph(quantize_all, reps=3)
     out["quantize_w3"] = {"ms": round(qms, 3),
                           "GBps": round(st.weights() * (2 + bytes_per_weight(3)) / (qms * 1e-3) / 1e9, 1)}
     log("stack32b:", out)
@@ -420,33 +439,34 @@ def main():
                                                 "GBps": round(stack.weight_bytes(bits) / (ms_b * 1e-3) / 1e9, 1)}
         extra["sweep"] = sweep
         log("sweep", sweep)
-        # quantize throughput over the whole stack (fp16 read + packed write)
+        # quantize throughput over the whole stack (fp16 read + packed write):
+        # all calls captured in one HIP graph (as the linear stack), and the
+        # same calls launched eagerly from Python for comparison
         qd = []
         for bits in (3, 4):
+            outs = stack.q[bits]
+
+            def quantize_all():
+                for i, w in enumerate(stack.fp16):
+                    laq.quantize(w, bits, out=outs[i])
+            qms = time_calls_graph(quantize_all)
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
-            outs = stack.q[bits]
-            for i, w in enumerate(stack.fp16):  # warm
-                laq.quantize(w, bits, out=outs[i])
-            torch.cuda.synchronize()
             e0.record()
-            for i, w in enumerate(stack.fp16):
-                laq.quantize(w, bits, out=outs[i])
+            quantize_all()
             e1.record()
             torch.cuda.synchronize()
-            qms = e0.elapsed_time(e1)
+            ems = e0.elapsed_time(e1)
             qbytes = stack.weights() * (2 + bytes_per_weight(bits))
-            qd.append(("w%d" % bits, {"ms": round(qms, 3), "GBps": round(qbytes / (qms * 1e-3) / 1e9, 1)}))
+            qd.append(("w%d" % bits, {"ms": round(qms, 3), "GBps": round(qbytes / (qms * 1e-3) / 1e9, 1),
+                                      "eager_ms": round(ems, 3)}))
         # pack with given parameters (the ones quantize just wrote), W3
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
         outs = stack.q[3]
-        e0.record()
-        for i, w in enumerate(stack.fp16):
-            laq.pack(w, outs[i][1], outs[i][2], 3, out=outs[i][0])
-        e1.record()
-        torch.cuda.synchronize()
-        pms = e0.elapsed_time(e1)
+
+        def pack_all():
+            for i, w in enumerate(stack.fp16):
+                laq.pack(w, outs[i][1], outs[i][2], 3, out=outs[i][0])
+        pms = time_calls_graph(pack_all)
         qd.append(("pack_w3", {"ms": round(pms, 3), "GBps": round(stack.weights() * (2 + bytes_per_weight(3)) / (pms * 1e-3) / 1e9, 1)}))
         extra["quantize_stack"] = dict(qd)
         log("quantize", extra["quantize_stack"])
