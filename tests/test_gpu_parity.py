@@ -582,3 +582,44 @@ def test_group_long_rows_one_row(bits):
     for y, y1, ref in zip(ys, singles, refs):
         assert linear_check(y, ref)["ok"]
         assert np.array_equal(y.view(np.uint16), y1.view(np.uint16))
+
+
+# ---------------------------------------------------------------------------
+# graph capture: every kernel path replayed several times, each replay equal
+# (bitwise) to the eager call, with eager work of the same kernels between
+# ---------------------------------------------------------------------------
+GRAPH_CASES = [
+    ("flat M=2 two rows per lane", 2, 300, 9728, 3),
+    ("matrix cores one tile M=5", 5, 1030, 4096, 4),
+    ("matrix cores four tiles M=16", 16, 16400, 2560, 3),
+    ("matrix cores walk M=8", 8, 16400, 4096, 3),
+    ("split K with workspace M=16", 16, 1030, 25600, 3),
+]
+
+
+@pytest.mark.parametrize("name,M,N,K,bits", GRAPH_CASES)
+def test_graph_replay(name, M, N, K, bits):
+    say("graph replay", name, M, N, K, bits)
+    w = to_dev(inputs.weights(N, K, cfg=21, layer=M))
+    x = to_dev(inputs.activations(M, K, cfg=21, layer=M))
+    q, s, z = laq.quantize(w, bits)
+    y_eager = laq.linear(x, q, s, z, bits)
+    torch.cuda.synchronize()
+    qg, sg, zg = torch.empty_like(q), torch.empty_like(s), torch.empty_like(z)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        laq.quantize(w, bits, out=(qg, sg, zg))
+        y_graph = laq.linear(x, qg, sg, zg, bits)
+    for _ in range(3):
+        for t in (qg, sg, zg, y_graph):
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(qg, q) and torch.equal(sg, s) and torch.equal(zg, z), name
+        assert torch.equal(y_graph.view(torch.int16), y_eager.view(torch.int16)), name
+        # eager work of the same kernels between replays
+        y2 = laq.linear(x, q, s, z, bits)
+        torch.cuda.synchronize()
+        assert torch.equal(y2.view(torch.int16), y_eager.view(torch.int16)), name
+    del g
