@@ -805,10 +805,11 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   }
   // (At most M tiles per wave: a wave's TW KiB of partials reuse its M KiB slab.)
   const int TW = min(M, tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1));
-  // One wave per quad of the row, at most 16 / TW (register budget) and as
-  // many M-row activation slabs (M KiB each) as fit in 160 KiB; longer rows
-  // loop.
-  const int wmax = min(16 / TW, kBlockLdsU4 / (M * kSlabRowU4));
+  // One wave per quad of the row, at most 8 (more waves per block measured
+  // slower: Qwen3-4B down, 19 quads, at M = 16 10.3 us with 10 waves, 10.0
+  // with 8) and as many M-row activation slabs (M KiB each) as fit in
+  // 160 KiB; longer rows loop.
+  const int wmax = min(8, kBlockLdsU4 / (M * kSlabRowU4));
   const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
   const int nblocks = (int)((tiles + TW - 1) / TW);
   const unsigned blocks = xcd_grid(nblocks);
