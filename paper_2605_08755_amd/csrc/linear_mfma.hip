@@ -841,7 +841,7 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
   }
   grp.count = count;
   grp.blocks = (int)blocks;
-  const int W = min(min(16, kBlockLdsU4 / (M * kSlabRowU4)), nq_max);
+  const int W = min(min(8, kBlockLdsU4 / (M * kSlabRowU4)), nq_max);  // as for one call
   launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * M * kSlabRowU4 * 16,
          stream, ev, grp, M);
   return hipGetLastError();
