@@ -262,6 +262,70 @@ laq_status laq_linear_ws_w4g128(const void *x, const uint32_t *qweight,
                                 void *workspace, int64_t workspace_bytes,
                                 void *stream);
 
+/* ------------------------------------------------------------------------
+ * Decode-step operations around the linears of a decoder layer (the model
+ * the paper quantizes and times, Sec. 5, Table 3), for one decode token.
+ * fp16 arrays are IEEE binary16; arithmetic is fp32 with fixed reduction
+ * orders (deterministic).  Head dimension 128.  Same conventions as above:
+ * host-side validation, nothing enqueued on error, asynchronous on `stream`,
+ * no allocation; outputs must not alias inputs unless stated.
+ * ------------------------------------------------------------------------ */
+
+/* laq_add_rmsnorm_f16 -- residual update and RMSNorm, row by row:
+ *   r = residual + delta;  y = fp16(r / sqrt(mean(r^2) + eps) * weight)
+ *   residual  [in/out] fp32 [M][D]; receives r (may be read by later calls).
+ *   delta     [in] fp16 [M][D], or NULL (then r = residual).
+ *   weight    [in] fp16 [D].   y [out] fp16 [M][D].
+ * Errors: NULL_POINTER; BAD_SHAPE (M < 1, D < 1, D > 2^20, eps < 0 or not
+ * finite); MISALIGNED (residual 4-byte, fp16 arrays 2-byte). */
+laq_status laq_add_rmsnorm_f16(float *residual, const void *delta, const void *weight, void *y,
+                               int64_t M, int64_t D, float eps, void *stream);
+
+/* laq_qk_norm_rope_f16 -- one token's fused q|k|v projection output
+ * qkv fp16 [(Hq + 2*Hkv) * 128] (q heads, then k heads, then v heads):
+ * every q and k head is RMS-normalized over its 128 values with its own
+ * weight vector (q_norm_weight / k_norm_weight, fp16 [128], eps as above),
+ * then rotated: pair (x_i, x_{i+64}), i < 64, becomes
+ * (x_i c_i - x_{i+64} s_i, x_{i+64} c_i + x_i s_i) with c_i, s_i read from
+ * row pos of cos_sin (fp32 [S_max][128]: the 64 cosines of pos * theta_i,
+ * then the 64 sines; the caller chooses the frequencies theta_i).  q heads go
+ * to q_out fp16 [Hq][128]; k and v heads to row pos of k_cache / v_cache,
+ * fp16 [Hkv][S_max][128] each (16-byte aligned).
+ * Errors: NULL_POINTER; BAD_SHAPE (head_dim != 128, Hq not Hkv times 1, 2, 4
+ * or 8, Hq > 4096, pos outside 0..S_max-1, S_max > 2^21, bad eps);
+ * MISALIGNED. */
+laq_status laq_qk_norm_rope_f16(const void *qkv, const void *q_norm_weight, const void *k_norm_weight,
+                                const float *cos_sin, int64_t pos, int64_t Hq, int64_t Hkv,
+                                int64_t head_dim, float eps, void *q_out, void *k_cache, void *v_cache,
+                                int64_t S_max, void *stream);
+
+/* laq_decode_attention_workspace_bytes -- workspace (bytes) that
+ * laq_decode_attention_f16 needs for Hq query heads over L positions
+ * (fp32 partial results per block of 64 positions); 0 for invalid sizes. */
+int64_t laq_decode_attention_workspace_bytes(int64_t Hq, int64_t L);
+
+/* laq_decode_attention_f16 -- single-token attention over the first L
+ * positions of the caches: query head h (q fp16 [Hq][128]) reads key/value
+ * head h / (Hq / Hkv);
+ *   out[h] = sum_t softmax_t(q[h] . k[t] / sqrt(128)) v[t]   (fp16 [Hq][128])
+ * Two kernels: partial results per block of 64 positions into the caller's
+ * workspace, then their combination in position order.
+ *   workspace  [scratch] device memory, 16-byte aligned, any contents, at
+ *              least laq_decode_attention_workspace_bytes(Hq, L) bytes; calls
+ *              in flight need separate workspaces.
+ * Errors: NULL_POINTER; BAD_SHAPE (head layout as above, L outside
+ * 1..S_max, S_max > 2^21, workspace too small); MISALIGNED. */
+laq_status laq_decode_attention_f16(const void *q, const void *k_cache, const void *v_cache, int64_t Hq,
+                                    int64_t Hkv, int64_t head_dim, int64_t L, int64_t S_max, void *out,
+                                    void *workspace, int64_t workspace_bytes, void *stream);
+
+/* laq_silu_mul_f16 -- y[m][i] = fp16(silu(g) * u), g = gate_up[m][i],
+ * u = gate_up[m][I + i], silu(g) = g / (1 + exp(-g)): the fused gate|up
+ * projection's output fp16 [M][2I] to the down projection's input
+ * fp16 [M][I].
+ * Errors: NULL_POINTER; BAD_SHAPE (M < 1, I < 1, M * I >= 2^38); MISALIGNED. */
+laq_status laq_silu_mul_f16(const void *gate_up, void *y, int64_t M, int64_t I, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

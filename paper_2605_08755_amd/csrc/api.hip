@@ -1,6 +1,7 @@
 // C ABI of the library (include/laq.h): argument validation on the host,
 // then an asynchronous launch on the caller's stream.  Nothing is enqueued
 // when validation fails.
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -222,6 +223,98 @@ laq_status laq_linear_w4g128(const void* x, const uint32_t* qweight, const void*
                              const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
                              void* stream) {
   return linear<4>("laq_linear_w4g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Decode-step operations
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int64_t kHeadDimAbi = 128;
+
+laq_status check_heads(const char* fn, int64_t Hq, int64_t Hkv, int64_t head_dim) {
+  if (head_dim != kHeadDimAbi) return fail(LAQ_ERR_BAD_SHAPE, fn, "head_dim must be 128");
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return fail(LAQ_ERR_BAD_SHAPE, fn, "Hq must be a positive multiple of Hkv");
+  const int64_t r = Hq / Hkv;
+  if (r != 1 && r != 2 && r != 4 && r != 8) return fail(LAQ_ERR_BAD_SHAPE, fn, "Hq / Hkv must be 1, 2, 4 or 8");
+  if (Hq > 4096) return fail(LAQ_ERR_BAD_SHAPE, fn, "Hq must be <= 4096");
+  return LAQ_OK;
+}
+}  // namespace
+
+extern "C" {
+
+laq_status laq_add_rmsnorm_f16(float* residual, const void* delta, const void* weight, void* y, int64_t M,
+                               int64_t D, float eps, void* stream) {
+  const char* fn = "laq_add_rmsnorm_f16";
+  const laq::LaunchEvents ev = take_events();
+  if (!residual || !weight || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  if (M < 1 || M > 0x7FFFFFFFLL || D < 1 || D > (1LL << 20)) return fail(LAQ_ERR_BAD_SHAPE, fn, "need 1 <= M < 2^31 and 1 <= D <= 2^20");
+  if (!(eps >= 0.0f) || !(eps < INFINITY)) return fail(LAQ_ERR_BAD_SHAPE, fn, "eps must be finite and >= 0");
+  if (!aligned(residual, 4) || !aligned(weight, 2) || !aligned(y, 2) || (delta && !aligned(delta, 2)))
+    return fail(LAQ_ERR_MISALIGNED, fn, "residual must be 4-byte, fp16 arrays 2-byte aligned");
+  return hip_status(fn, laq::launch_add_rmsnorm(residual, static_cast<const uint16_t*>(delta),
+                                                static_cast<const uint16_t*>(weight), static_cast<uint16_t*>(y), M, D,
+                                                eps, static_cast<hipStream_t>(stream), ev));
+}
+
+laq_status laq_qk_norm_rope_f16(const void* qkv, const void* q_norm_weight, const void* k_norm_weight,
+                                const float* cos_sin, int64_t pos, int64_t Hq, int64_t Hkv, int64_t head_dim,
+                                float eps, void* q_out, void* k_cache, void* v_cache, int64_t S_max, void* stream) {
+  const char* fn = "laq_qk_norm_rope_f16";
+  const laq::LaunchEvents ev = take_events();
+  if (!qkv || !q_norm_weight || !k_norm_weight || !cos_sin || !q_out || !k_cache || !v_cache)
+    return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_heads(fn, Hq, Hkv, head_dim);
+  if (st != LAQ_OK) return st;
+  if (S_max < 1 || S_max > (1LL << 21) || pos < 0 || pos >= S_max)
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need 1 <= S_max <= 2^21 and 0 <= pos < S_max");
+  if (!(eps >= 0.0f) || !(eps < INFINITY)) return fail(LAQ_ERR_BAD_SHAPE, fn, "eps must be finite and >= 0");
+  if (!aligned(qkv, 2) || !aligned(q_norm_weight, 2) || !aligned(k_norm_weight, 2) || !aligned(cos_sin, 4) ||
+      !aligned(q_out, 2) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
+    return fail(LAQ_ERR_MISALIGNED, fn, "caches must be 16-byte, cos_sin 4-byte, fp16 arrays 2-byte aligned");
+  return hip_status(fn, laq::launch_qk_norm_rope(
+                            static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(q_norm_weight),
+                            static_cast<const uint16_t*>(k_norm_weight), cos_sin, pos, Hq, Hkv, eps,
+                            static_cast<uint16_t*>(q_out), static_cast<uint16_t*>(k_cache),
+                            static_cast<uint16_t*>(v_cache), S_max, static_cast<hipStream_t>(stream), ev));
+}
+
+int64_t laq_decode_attention_workspace_bytes(int64_t Hq, int64_t L) {
+  if (Hq < 1 || L < 1 || Hq > 4096 || L > (1LL << 21)) return 0;
+  return Hq * laq::decode_attention_tiles(L) * (kHeadDimAbi + 2) * (int64_t)sizeof(float);
+}
+
+laq_status laq_decode_attention_f16(const void* q, const void* k_cache, const void* v_cache, int64_t Hq,
+                                    int64_t Hkv, int64_t head_dim, int64_t L, int64_t S_max, void* out,
+                                    void* workspace, int64_t workspace_bytes, void* stream) {
+  const char* fn = "laq_decode_attention_f16";
+  const laq::LaunchEvents ev = take_events();
+  if (!q || !k_cache || !v_cache || !out || !workspace) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_heads(fn, Hq, Hkv, head_dim);
+  if (st != LAQ_OK) return st;
+  if (S_max < 1 || S_max > (1LL << 21) || L < 1 || L > S_max)
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need 1 <= L <= S_max <= 2^21");
+  if (workspace_bytes < laq_decode_attention_workspace_bytes(Hq, L))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "workspace_bytes below laq_decode_attention_workspace_bytes(Hq, L)");
+  if (!aligned(q, 2) || !aligned(out, 2) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(workspace, 16))
+    return fail(LAQ_ERR_MISALIGNED, fn, "caches and workspace must be 16-byte, q and out 2-byte aligned");
+  return hip_status(fn, laq::launch_decode_attention(
+                            static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
+                            static_cast<const uint16_t*>(v_cache), Hq, Hkv, L, S_max, static_cast<uint16_t*>(out),
+                            static_cast<float*>(workspace), static_cast<hipStream_t>(stream), ev));
+}
+
+laq_status laq_silu_mul_f16(const void* gate_up, void* y, int64_t M, int64_t I, void* stream) {
+  const char* fn = "laq_silu_mul_f16";
+  const laq::LaunchEvents ev = take_events();
+  if (!gate_up || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  if (M < 1 || I < 1 || M > 0x7FFFFFFFLL || I > (1LL << 30) || M * I >= (1LL << 38))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need M, I >= 1 and M * I < 2^38");
+  if (!aligned(gate_up, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "fp16 arrays must be 2-byte aligned");
+  return hip_status(fn, laq::launch_silu_mul(static_cast<const uint16_t*>(gate_up), static_cast<uint16_t*>(y), M, I,
+                                             static_cast<hipStream_t>(stream), ev));
 }
 
 }  // extern "C"

@@ -129,4 +129,17 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
                          hipStream_t stream, const LaunchEvents& ev, float* workspace = nullptr,
                          size_t workspace_bytes = 0);
 
+// Decode-step operations (decode.hip); head dimension 128.
+int64_t decode_attention_tiles(int64_t L);
+hipError_t launch_add_rmsnorm(float* res, const uint16_t* delta, const uint16_t* w, uint16_t* y, int64_t M,
+                              int64_t D, float eps, hipStream_t stream, const LaunchEvents& ev);
+hipError_t launch_qk_norm_rope(const uint16_t* qkv, const uint16_t* qw, const uint16_t* kw, const float* cos_sin,
+                               int64_t pos, int64_t Hq, int64_t Hkv, float eps, uint16_t* q_out, uint16_t* kc,
+                               uint16_t* vc, int64_t S_max, hipStream_t stream, const LaunchEvents& ev);
+hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, int64_t Hq,
+                                   int64_t Hkv, int64_t L, int64_t S_max, uint16_t* out, float* ws,
+                                   hipStream_t stream, const LaunchEvents& ev);
+hipError_t launch_silu_mul(const uint16_t* gu, uint16_t* y, int64_t M, int64_t I, hipStream_t stream,
+                           const LaunchEvents& ev);
+
 }  // namespace laq

@@ -25,7 +25,10 @@ MAX_GROUP = 8
 EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profile_next_launch",
            "laq_quantize_w3g128", "laq_pack_w3g128", "laq_linear_w3g128", "laq_linear_group_w3g128",
            "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128", "laq_linear_group_w4g128",
-           "laq_linear_workspace_bytes", "laq_linear_ws_w3g128", "laq_linear_ws_w4g128")
+           "laq_linear_workspace_bytes", "laq_linear_ws_w3g128", "laq_linear_ws_w4g128",
+           "laq_add_rmsnorm_f16", "laq_qk_norm_rope_f16", "laq_decode_attention_workspace_bytes",
+           "laq_decode_attention_f16", "laq_silu_mul_f16")
+HEAD_DIM = 128
 
 
 class LinearCall(ctypes.Structure):
@@ -81,6 +84,17 @@ def lib():
             f.restype = ctypes.c_int32
         L.laq_linear_workspace_bytes.argtypes = [I64, I64, I64]
         L.laq_linear_workspace_bytes.restype = I64
+        F32 = ctypes.c_float
+        L.laq_add_rmsnorm_f16.argtypes = [P, P, P, P, I64, I64, F32, P]
+        L.laq_add_rmsnorm_f16.restype = ctypes.c_int32
+        L.laq_qk_norm_rope_f16.argtypes = [P, P, P, P, I64, I64, I64, I64, F32, P, P, P, I64, P]
+        L.laq_qk_norm_rope_f16.restype = ctypes.c_int32
+        L.laq_decode_attention_workspace_bytes.argtypes = [I64, I64]
+        L.laq_decode_attention_workspace_bytes.restype = I64
+        L.laq_decode_attention_f16.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, P, I64, P]
+        L.laq_decode_attention_f16.restype = ctypes.c_int32
+        L.laq_silu_mul_f16.argtypes = [P, P, I64, I64, P]
+        L.laq_silu_mul_f16.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -229,3 +243,72 @@ def quantize_w4g128(w, out=None):
 
 def linear_w4g128(x, qweight, scales, zeros, out=None):
     return linear(x, qweight, scales, zeros, 4, out)
+
+
+# ---------------------------------------------------------------------------
+# decode-step operations (one token; head dimension 128)
+# ---------------------------------------------------------------------------
+def add_rmsnorm(residual, delta, weight, eps, out=None):
+    """residual (fp32 [M][D], updated in place) += delta (fp16 [M][D] or None);
+    returns fp16 RMSNorm(residual) * weight."""
+    import torch
+    assert residual.is_cuda and residual.dtype == torch.float32 and residual.dim() == 2 and residual.is_contiguous()
+    M, D = residual.shape
+    assert weight.dtype == torch.float16 and weight.numel() == D and weight.is_contiguous()
+    if delta is not None:
+        assert delta.dtype == torch.float16 and delta.shape == (M, D) and delta.is_contiguous()
+    if out is None:
+        out = torch.empty((M, D), dtype=torch.float16, device=residual.device)
+    _check(lib().laq_add_rmsnorm_f16(_ptr(residual), _ptr(delta) if delta is not None else None, _ptr(weight),
+                                     _ptr(out), M, D, float(eps), _stream(residual.device)))
+    return out
+
+
+def qk_norm_rope(qkv, q_norm_weight, k_norm_weight, cos_sin, pos, Hq, Hkv, eps, k_cache, v_cache, q_out=None):
+    """One token's q|k|v projection output -> normalized, rotated q (returned,
+    fp16 [Hq][128]); k and v written to row pos of the caches [Hkv][S_max][128]."""
+    import torch
+    assert qkv.is_cuda and qkv.dtype == torch.float16 and qkv.is_contiguous() and qkv.numel() == (Hq + 2 * Hkv) * HEAD_DIM
+    assert cos_sin.dtype == torch.float32 and cos_sin.dim() == 2 and cos_sin.shape[1] == HEAD_DIM and cos_sin.is_contiguous()
+    S_max = k_cache.shape[1]
+    assert k_cache.shape == (Hkv, S_max, HEAD_DIM) and v_cache.shape == k_cache.shape and cos_sin.shape[0] >= S_max
+    assert k_cache.dtype == torch.float16 and v_cache.dtype == torch.float16
+    if q_out is None:
+        q_out = torch.empty((Hq, HEAD_DIM), dtype=torch.float16, device=qkv.device)
+    _check(lib().laq_qk_norm_rope_f16(_ptr(qkv), _ptr(q_norm_weight), _ptr(k_norm_weight), _ptr(cos_sin), int(pos),
+                                      Hq, Hkv, HEAD_DIM, float(eps), _ptr(q_out), _ptr(k_cache), _ptr(v_cache), S_max,
+                                      _stream(qkv.device)))
+    return q_out
+
+
+def attention_workspace_bytes(Hq, L):
+    return int(lib().laq_decode_attention_workspace_bytes(Hq, L))
+
+
+def decode_attention(q, k_cache, v_cache, L, out=None, workspace=None):
+    """Single-token attention over the first L cache positions; returns fp16 [Hq][128]."""
+    import torch
+    Hq = q.shape[0]
+    Hkv, S_max, d = k_cache.shape
+    assert q.dtype == torch.float16 and q.shape == (Hq, HEAD_DIM) and q.is_contiguous() and d == HEAD_DIM
+    if out is None:
+        out = torch.empty((Hq, HEAD_DIM), dtype=torch.float16, device=q.device)
+    need = attention_workspace_bytes(Hq, L)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _check(lib().laq_decode_attention_f16(_ptr(q), _ptr(k_cache), _ptr(v_cache), Hq, Hkv, HEAD_DIM, int(L), S_max,
+                                          _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                          _stream(q.device)))
+    return out
+
+
+def silu_mul(gate_up, out=None):
+    """fp16 [M][2I] gate | up -> fp16 [M][I] silu(gate) * up."""
+    import torch
+    assert gate_up.is_cuda and gate_up.dtype == torch.float16 and gate_up.dim() == 2 and gate_up.is_contiguous()
+    M, I2 = gate_up.shape
+    assert I2 % 2 == 0
+    if out is None:
+        out = torch.empty((M, I2 // 2), dtype=torch.float16, device=gate_up.device)
+    _check(lib().laq_silu_mul_f16(_ptr(gate_up), _ptr(out), M, I2 // 2, _stream(gate_up.device)))
+    return out

@@ -188,3 +188,70 @@ def test_packed_sizes():
     # 32 three-bit codes in three words: N*K*3/32 words; W4: N*K/8 words
     assert laq.packed_words(3, 1024, 1024) * 4 == 1024 * 1024 * 3 // 8
     assert laq.packed_words(4, 1024, 1024) * 4 == 1024 * 1024 // 2
+
+
+# --- decode-step operations -------------------------------------------------
+def _norm(L, r=FAKE, d=FAKE, w=FAKE, y=FAKE, M=1, D=2560, eps=1e-6):
+    return L.laq_add_rmsnorm_f16(ctypes.c_void_p(r), ctypes.c_void_p(d) if d else None, ctypes.c_void_p(w),
+                                 ctypes.c_void_p(y), M, D, eps, None)
+
+
+def _rope(L, qkv=FAKE, qw=FAKE, kw=FAKE, cs=FAKE, pos=0, Hq=32, Hkv=8, hd=128, eps=1e-6, q=FAKE, kc=FAKE,
+          vc=FAKE, S=1024):
+    return L.laq_qk_norm_rope_f16(ctypes.c_void_p(qkv), ctypes.c_void_p(qw), ctypes.c_void_p(kw), ctypes.c_void_p(cs),
+                                  pos, Hq, Hkv, hd, eps, ctypes.c_void_p(q), ctypes.c_void_p(kc), ctypes.c_void_p(vc),
+                                  S, None)
+
+
+def _attn(L, q=FAKE, kc=FAKE, vc=FAKE, Hq=32, Hkv=8, hd=128, Lp=100, S=1024, out=FAKE, ws=FAKE, wsb=1 << 20):
+    return L.laq_decode_attention_f16(ctypes.c_void_p(q), ctypes.c_void_p(kc), ctypes.c_void_p(vc), Hq, Hkv, hd, Lp,
+                                      S, ctypes.c_void_p(out), ctypes.c_void_p(ws), wsb, None)
+
+
+def test_decode_ops_validation(L):
+    for kw in ("r", "w", "y"):
+        assert _norm(L, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _norm(L, M=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _norm(L, D=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _norm(L, D=(1 << 20) + 1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _norm(L, eps=-1.0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _norm(L, eps=float("nan")) == laq.LAQ_ERR_BAD_SHAPE
+    assert _norm(L, r=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert _norm(L, d=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_add_rmsnorm_f16" in L.laq_last_error()
+
+    for kw in ("qkv", "qw", "kw", "cs", "q", "kc", "vc"):
+        assert _rope(L, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _rope(L, hd=64) == laq.LAQ_ERR_BAD_SHAPE
+    assert _rope(L, Hq=24) == laq.LAQ_ERR_BAD_SHAPE      # ratio 3
+    assert _rope(L, Hq=128) == laq.LAQ_ERR_BAD_SHAPE     # ratio 16
+    assert _rope(L, Hkv=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _rope(L, pos=1024) == laq.LAQ_ERR_BAD_SHAPE
+    assert _rope(L, pos=-1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _rope(L, S=(1 << 21) + 1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _rope(L, kc=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert _rope(L, cs=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_qk_norm_rope_f16" in L.laq_last_error()
+
+    for kw in ("q", "kc", "vc", "out", "ws"):
+        assert _attn(L, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _attn(L, hd=256) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn(L, Hq=40) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn(L, Lp=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn(L, Lp=1025) == laq.LAQ_ERR_BAD_SHAPE
+    need = L.laq_decode_attention_workspace_bytes(32, 100)
+    assert need == 32 * 2 * 130 * 4  # two blocks of 64 positions, (m, l, 128 sums) in fp32
+    assert _attn(L, wsb=need - 1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn(L, ws=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert _attn(L, vc=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_decode_attention_f16" in L.laq_last_error()
+    assert L.laq_decode_attention_workspace_bytes(0, 5) == 0
+    assert L.laq_decode_attention_workspace_bytes(8, 64) == 8 * 1 * 130 * 4
+    assert L.laq_decode_attention_workspace_bytes(8, 65) == 8 * 2 * 130 * 4
+
+    f = L.laq_silu_mul_f16
+    assert f(None, ctypes.c_void_p(FAKE), 1, 8, None) == laq.LAQ_ERR_NULL_POINTER
+    assert f(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0, 8, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 1, 0, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(ctypes.c_void_p(FAKE + 1), ctypes.c_void_p(FAKE), 1, 8, None) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_silu_mul_f16" in L.laq_last_error()
