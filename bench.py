@@ -242,6 +242,48 @@ def time_fp16_graph(stack, M, steps, warmup):
     return ms
 
 
+def decode_step_extra(stack, dev, steps, context=1024):
+    """One batch-1 decode step of the Qwen3-4B-shaped decoder (36 layers:
+    norms, rotary embedding, attention over a synthetic KV cache of `context`
+    positions, SiLU-and-multiply, and the stack's linears), the token at
+    position context - 1, captured in a HIP graph: with the W3 linears, and
+    with the fp16 weights through torch's dense GEMM for the unquantized
+    reference.  The LM head is not part of the step."""
+    import torch
+    from paper_2605_08755_amd import decode, inputs, laq
+    shape = dict(decode.QWEN3_4B)
+    assert stack.workload == "stack4b" and len(stack.shapes) == 4 * shape["layers"]
+    g = torch.Generator(device=dev)
+    g.manual_seed(inputs.ENTROPY * 1000 + 900000)
+
+    def vec(n):
+        return (1.0 + 0.1 * torch.randn((n,), generator=g, device=dev)).to(torch.float16)
+
+    D, Hkv = shape["hidden"], shape["kv_heads"]
+    norms = [(vec(D), vec(D), vec(128), vec(128)) for _ in range(shape["layers"])]
+    caches = [torch.randn((2, Hkv, context, 128), generator=g, device=dev).to(torch.float16)
+              for _ in range(shape["layers"])]
+
+    def w3_lin(i):
+        q, sc, z = stack.q[3][i]
+        return lambda x, out: laq.linear(x, q, sc, z, 3, out=out)
+
+    def fp16_lin(i):
+        w = stack.fp16[i]
+        return lambda x, out: torch.mm(x, w.t(), out=out)
+
+    out = {"context": context, "layers": shape["layers"]}
+    for name, mk in (("w3", w3_lin), ("fp16", fp16_lin)):
+        lins = [tuple(mk(4 * l + j) for j in range(4)) for l in range(shape["layers"])]
+        step = decode.DecodeStep(shape, lins, norms, vec(D), [c[0] for c in caches], [c[1] for c in caches], dev)
+        step.x0.copy_(torch.randn((1, D), generator=g, device=dev))
+        ms, _ = time_graph(stack, 1, 3, steps, 5, step_fn=lambda: step.run(context - 1))
+        out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}
+        del step
+    out["w3_speedup_vs_fp16"] = round(out["fp16"]["us"] / out["w3"]["us"], 3)
+    return out
+
+
 def stack32b_extra(dev, steps):
     """The 64-layer Qwen3-32B-shaped stack: W3 decode-step time at M = 1 and
     16, and quantize throughput over all of its fp16 weights."""
@@ -479,6 +521,9 @@ def main():
                              "w3_speedup": round(fms * 1e3 / w3, 3)}
         extra["fp16_dense_torch"] = fp
         log("fp16 dense (torch.mm):", fp)
+        if args.workload == "stack4b":
+            extra["decode_step_4b"] = decode_step_extra(stack, dev, max(20, args.steps // 4))
+            log("decode step:", extra["decode_step_4b"])
 
     if not args.no_sweep:
         stack.fp16 = None  # free the 4B stack's tensors; its shapes stay for the report

@@ -323,7 +323,8 @@ laq_status laq_decode_attention_f16(const void *q, const void *k_cache, const vo
  * u = gate_up[m][I + i], silu(g) = g / (1 + exp(-g)): the fused gate|up
  * projection's output fp16 [M][2I] to the down projection's input
  * fp16 [M][I].
- * Errors: NULL_POINTER; BAD_SHAPE (M < 1, I < 1, M * I >= 2^38); MISALIGNED. */
+ * Errors: NULL_POINTER; BAD_SHAPE (M outside 1..65535, I outside 1..2^30);
+ * MISALIGNED. */
 laq_status laq_silu_mul_f16(const void *gate_up, void *y, int64_t M, int64_t I, void *stream);
 
 #ifdef __cplusplus

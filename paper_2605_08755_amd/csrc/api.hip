@@ -310,8 +310,8 @@ laq_status laq_silu_mul_f16(const void* gate_up, void* y, int64_t M, int64_t I, 
   const char* fn = "laq_silu_mul_f16";
   const laq::LaunchEvents ev = take_events();
   if (!gate_up || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
-  if (M < 1 || I < 1 || M > 0x7FFFFFFFLL || I > (1LL << 30) || M * I >= (1LL << 38))
-    return fail(LAQ_ERR_BAD_SHAPE, fn, "need M, I >= 1 and M * I < 2^38");
+  if (M < 1 || I < 1 || M > 65535 || I > (1LL << 30))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need 1 <= M <= 65535 and 1 <= I <= 2^30");
   if (!aligned(gate_up, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "fp16 arrays must be 2-byte aligned");
   return hip_status(fn, laq::launch_silu_mul(static_cast<const uint16_t*>(gate_up), static_cast<uint16_t*>(y), M, I,
                                              static_cast<hipStream_t>(stream), ev));

@@ -33,6 +33,11 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // One row per block: r = residual + delta (written back), y = r / rms(r) * w.
+// Rows of up to 16 elements per thread take one pass: every load is issued
+// (indices clamped into the row, so no branch stands between loads) before
+// any arithmetic, and r stays in registers.  HAS_DELTA: delta is not null.
+constexpr int kNormRegs = 16;
+template <bool HAS_DELTA>
 __global__ __launch_bounds__(kNormThreads) void add_rmsnorm_kernel(float* __restrict__ res,
                                                                    const uint16_t* __restrict__ delta,
                                                                    const uint16_t* __restrict__ w,
@@ -40,23 +45,54 @@ __global__ __launch_bounds__(kNormThreads) void add_rmsnorm_kernel(float* __rest
   __shared__ float part[kNormThreads / 64];
   const int64_t row = blockIdx.x;
   float* r = res + row * D;
-  const uint16_t* dl = delta ? delta + row * D : nullptr;
+  const uint16_t* dl = HAS_DELTA ? delta + row * D : nullptr;
   uint16_t* yr = y + row * D;
+  const int t = threadIdx.x;
   float ss = 0.0f;
-  for (int i = threadIdx.x; i < D; i += kNormThreads) {
+  if (D <= kNormRegs * kNormThreads) {
+    float v[kNormRegs], wv[kNormRegs], dv[kNormRegs];
+#pragma unroll
+    for (int k = 0; k < kNormRegs; ++k) {
+      const int i = min(t + k * kNormThreads, D - 1);
+      v[k] = r[i];
+      wv[k] = h2f(w[i]);
+      dv[k] = HAS_DELTA ? h2f(dl[i]) : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < kNormRegs; ++k) {
+      const bool in = t + k * kNormThreads < D;
+      v[k] = in ? v[k] + dv[k] : 0.0f;
+      ss = fmaf(v[k], v[k], ss);
+    }
+#pragma unroll
+    for (int k = 0; k < kNormRegs; ++k)
+      if (t + k * kNormThreads < D) r[t + k * kNormThreads] = v[k];
+    ss = wave_sum(ss);
+    if ((t & 63) == 0) part[t >> 6] = ss;
+    __syncthreads();
+    float tot = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kNormThreads / 64; ++i) tot += part[i];
+    const float inv = 1.0f / sqrtf(tot / (float)D + eps);
+#pragma unroll
+    for (int k = 0; k < kNormRegs; ++k)
+      if (t + k * kNormThreads < D) yr[t + k * kNormThreads] = f2h(v[k] * inv * wv[k]);
+    return;
+  }
+  for (int i = t; i < D; i += kNormThreads) {
     float v = r[i];
-    if (dl) v += h2f(dl[i]);
+    if (HAS_DELTA) v += h2f(dl[i]);
     r[i] = v;
     ss = fmaf(v, v, ss);
   }
   ss = wave_sum(ss);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
+  if ((t & 63) == 0) part[t >> 6] = ss;
   __syncthreads();
   float tot = 0.0f;
 #pragma unroll
   for (int i = 0; i < kNormThreads / 64; ++i) tot += part[i];
   const float inv = 1.0f / sqrtf(tot / (float)D + eps);
-  for (int i = threadIdx.x; i < D; i += kNormThreads) yr[i] = f2h(r[i] * inv * h2f(w[i]));
+  for (int i = t; i < D; i += kNormThreads) yr[i] = f2h(r[i] * inv * h2f(w[i]));
 }
 
 // One head per block (64 lanes; lane i holds dimensions i and i + 64, the
@@ -93,104 +129,136 @@ __global__ __launch_bounds__(64) void qk_norm_rope_kernel(const uint16_t* __rest
   dst[i + 64] = f2h(b * c + a * s);
 }
 
-// Partial attention of one key/value head over 64 positions (one wave):
-// lane t scores position 64*tile + t against the R query heads of the group,
-// then the softmax statistics (max m, sum l of exp(s - m)) and the weighted
-// value sums o (lane i: dimensions i and i + 64) go to the workspace,
-// ws[((h * T) + tile) * 130 + {0: m, 1: l, 2..129: o}].
+// Partial attention of one key/value head over 64 positions: a block of R
+// waves, wave w for query head g*R + w of the group.  The block loads the
+// tile's key and value rows (16 KiB each, contiguous) into LDS with
+// coalesced 16-byte loads, all issued before the first is used; rows past L
+// read zero (buffer extent).  Lane t then scores position 64*tile + t, the
+// wave forms its softmax statistics (max m, sum l of exp(s - m)) and the
+// weighted value sums o (lane i: dimensions i and i + 64), written to
+// ws[((h * T) + tile) * 130 + {0: m, 1: l, 2..129: o}].  Key rows sit in LDS
+// with a 16-byte pad (a stride of 17 units), so that lanes reading their own
+// rows spread over the banks.
+constexpr int kKeyStrideU4 = kHeadDim / 8 + 1;
 template <int R>
-__global__ __launch_bounds__(64) void attn_partial_kernel(const uint16_t* __restrict__ q,
-                                                          const uint16_t* __restrict__ kc,
-                                                          const uint16_t* __restrict__ vc, int64_t S_max,
-                                                          int L, int T, float* __restrict__ ws) {
+__global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __restrict__ q,
+                                                              const uint16_t* __restrict__ kc,
+                                                              const uint16_t* __restrict__ vc, int64_t S_max,
+                                                              int L, int T, float* __restrict__ ws) {
   __shared__ float qs[R][kHeadDim];
+  __shared__ u32x4 kt[kAttnTile * kKeyStrideU4];
+  __shared__ u32x4 vt[kAttnTile * kHeadDim / 8];
+  constexpr int kUnits = kAttnTile * kHeadDim / 8;  // 16-byte units per tile
+  constexpr int kPer = kUnits / (64 * R);           // per thread
   const int g = blockIdx.x;
   const int tile = blockIdx.y;
-  const int lane = threadIdx.x;
-  const int p = tile * kAttnTile + lane;
-  const bool valid = p < L;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int npos = min(kAttnTile, L - tile * kAttnTile);
+  const int64_t row0 = (int64_t)g * S_max + (int64_t)tile * kAttnTile;
+  const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kc + row0 * kHeadDim),
+                                                                     (short)0, npos * kHeadDim * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(vc + row0 * kHeadDim),
+                                                                     (short)0, npos * kHeadDim * 2, 0x00020000);
+  u32x4 ka[kPer], va[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const uint32_t u = (uint32_t)(i * 64 * R + tid);
+    ka[i] = __builtin_amdgcn_raw_buffer_load_b128(kr, u * 16, 0, 0);
+    va[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, u * 16, 0, 0);
+  }
   const float scale = 0.08838834764831845f;  // 1 / sqrt(128)
-  for (int k = lane; k < R * kHeadDim; k += 64)
+  for (int k = tid; k < R * kHeadDim; k += 64 * R)
     qs[k / kHeadDim][k % kHeadDim] = h2f(q[((int64_t)g * R) * kHeadDim + k]) * scale;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = i * 64 * R + tid;
+    kt[(u >> 4) * kKeyStrideU4 + (u & 15)] = ka[i];
+    vt[u] = va[i];
+  }
   __syncthreads();
 
-  float s[R];
+  const int p = tile * kAttnTile + lane;
+  const bool valid = p < L;
+  float sc = 0.0f;
 #pragma unroll
-  for (int r = 0; r < R; ++r) s[r] = 0.0f;
-  const uint16_t* krow = kc + ((int64_t)g * S_max + (valid ? p : 0)) * kHeadDim;
-#pragma unroll 4
   for (int c = 0; c < kHeadDim / 8; ++c) {
-    const u32x4 kv = *reinterpret_cast<const u32x4*>(krow + c * 8);
+    const u32x4 kv = kt[lane * kKeyStrideU4 + c];
     const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float kf = h2f((uint16_t)(wv[e >> 1] >> (16 * (e & 1))));
-#pragma unroll
-      for (int r = 0; r < R; ++r) s[r] = fmaf(kf, qs[r][c * 8 + e], s[r]);
-    }
+    for (int e = 0; e < 8; ++e)
+      sc = fmaf(h2f((uint16_t)(wv[e >> 1] >> (16 * (e & 1)))), qs[w][c * 8 + e], sc);
   }
-  float m[R], l[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const float sv = valid ? s[r] : -INFINITY;
-    m[r] = wave_max(sv);
-    s[r] = valid ? expf(sv - m[r]) : 0.0f;
-    l[r] = wave_sum(s[r]);
+  const float sv = valid ? sc : -INFINITY;
+  const float m = wave_max(sv);
+  const float pr = valid ? expf(sv - m) : 0.0f;
+  const float l = wave_sum(pr);
+  float o0 = 0.0f, o1 = 0.0f;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(vt);
+  for (int t = 0; t < npos; ++t) {
+    const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pr), t));
+    o0 = fmaf(pt, h2f(vh[t * kHeadDim + lane]), o0);
+    o1 = fmaf(pt, h2f(vh[t * kHeadDim + lane + 64]), o1);
   }
-  float o0[R], o1[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) o0[r] = o1[r] = 0.0f;
-  const uint16_t* vrow = vc + ((int64_t)g * S_max + (int64_t)tile * kAttnTile) * kHeadDim;
-  const int npos = min(kAttnTile, L - tile * kAttnTile);
-  for (int t = 0; t < npos; ++t, vrow += kHeadDim) {
-    const float v0 = h2f(vrow[lane]), v1 = h2f(vrow[lane + 64]);
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, s[r]), t));
-      o0[r] = fmaf(pt, v0, o0[r]);
-      o1[r] = fmaf(pt, v1, o1[r]);
-    }
+  float* wp = ws + ((int64_t)(g * R + w) * T + tile) * (kHeadDim + 2);
+  if (lane == 0) {
+    wp[0] = m;
+    wp[1] = l;
   }
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    float* wp = ws + ((int64_t)(g * R + r) * T + tile) * (kHeadDim + 2);
-    if (lane == 0) {
-      wp[0] = m[r];
-      wp[1] = l[r];
-    }
-    wp[2 + lane] = o0[r];
-    wp[2 + 64 + lane] = o1[r];
-  }
+  wp[2 + lane] = o0;
+  wp[2 + 64 + lane] = o1;
 }
 
-// Combines the T partials of each query head in tile order.
-__global__ __launch_bounds__(kHeadDim) void attn_combine_kernel(const float* __restrict__ ws, int T,
-                                                                 uint16_t* __restrict__ out) {
+// Combines the T partials of each query head in tile order: one wave per
+// head; the per-tile weights exp(m_t - M) are computed by lane t (batches of
+// 64 tiles), and each lane adds dimensions i and i + 64 over the tiles with
+// eight partial rows loaded at a time.
+__global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restrict__ ws, int T,
+                                                          uint16_t* __restrict__ out) {
   const int h = blockIdx.x;
-  const int d = threadIdx.x;
+  const int lane = threadIdx.x;
   const float* base = ws + (int64_t)h * T * (kHeadDim + 2);
   float M = -INFINITY;
-  for (int t = 0; t < T; ++t) M = fmaxf(M, base[(int64_t)t * (kHeadDim + 2)]);
-  float num = 0.0f, den = 0.0f;
-  for (int t = 0; t < T; ++t) {
-    const float* pt = base + (int64_t)t * (kHeadDim + 2);
-    const float e = expf(pt[0] - M);
-    den = fmaf(e, pt[1], den);
-    num = fmaf(e, pt[2 + d], num);
+  for (int t0 = 0; t0 < T; t0 += 64)
+    M = fmaxf(M, wave_max(t0 + lane < T ? base[(int64_t)(t0 + lane) * (kHeadDim + 2)] : -INFINITY));
+  float den = 0.0f, n0 = 0.0f, n1 = 0.0f;
+  for (int t0 = 0; t0 < T; t0 += 64) {
+    const int t = t0 + lane;
+    const float e = t < T ? expf(base[(int64_t)t * (kHeadDim + 2)] - M) : 0.0f;
+    den += wave_sum(t < T ? e * base[(int64_t)t * (kHeadDim + 2) + 1] : 0.0f);
+    const int nt = min(64, T - t0);
+    for (int j0 = 0; j0 < nt; j0 += 8) {
+      float a0[8], a1[8], ej[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int jj = min(j0 + j, nt - 1);
+        const float* pt = base + (int64_t)(t0 + jj) * (kHeadDim + 2) + 2;
+        a0[j] = pt[lane];
+        a1[j] = pt[lane + 64];
+        ej[j] = (j0 + j < nt) ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, e), jj)) : 0.0f;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        n0 = fmaf(ej[j], a0[j], n0);
+        n1 = fmaf(ej[j], a1[j], n1);
+      }
+    }
   }
-  out[(int64_t)h * kHeadDim + d] = f2h(num / den);
+  out[(int64_t)h * kHeadDim + lane] = f2h(n0 / den);
+  out[(int64_t)h * kHeadDim + lane + 64] = f2h(n1 / den);
 }
 
-// y[m][i] = silu(g) * u with g = gu[m][i], u = gu[m][I + i].
+
+// y[m][i] = silu(g) * u with g = gu[m][i], u = gu[m][I + i]; row m = blockIdx.y.
 __global__ __launch_bounds__(256) void silu_mul_kernel(const uint16_t* __restrict__ gu, uint16_t* __restrict__ y,
-                                                       int64_t M, int64_t I) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= M * I) return;
-  const int64_t m = idx / I;
-  const int64_t i = idx - m * I;
+                                                       int64_t I) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= I) return;
+  const int64_t m = blockIdx.y;
   const float g = h2f(gu[m * 2 * I + i]);
   const float u = h2f(gu[m * 2 * I + I + i]);
-  y[idx] = f2h(g / (1.0f + expf(-g)) * u);
+  y[m * I + i] = f2h(g / (1.0f + expf(-g)) * u);
 }
 
 }  // namespace
@@ -199,7 +267,10 @@ int64_t decode_attention_tiles(int64_t L) { return (L + kAttnTile - 1) / kAttnTi
 
 hipError_t launch_add_rmsnorm(float* res, const uint16_t* delta, const uint16_t* w, uint16_t* y, int64_t M,
                               int64_t D, float eps, hipStream_t stream, const LaunchEvents& ev) {
-  launch(add_rmsnorm_kernel, dim3((unsigned)M), dim3(kNormThreads), 0, stream, ev, res, delta, w, y, (int)D, eps);
+  if (delta)
+    launch(add_rmsnorm_kernel<true>, dim3((unsigned)M), dim3(kNormThreads), 0, stream, ev, res, delta, w, y, (int)D, eps);
+  else
+    launch(add_rmsnorm_kernel<false>, dim3((unsigned)M), dim3(kNormThreads), 0, stream, ev, res, delta, w, y, (int)D, eps);
   return hipGetLastError();
 }
 
@@ -222,18 +293,17 @@ hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kc, const 
   const dim3 grid((unsigned)Hkv, (unsigned)T);
   switch (R) {
     case 1: launch(attn_partial_kernel<1>, grid, dim3(64), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
-    case 2: launch(attn_partial_kernel<2>, grid, dim3(64), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
-    case 4: launch(attn_partial_kernel<4>, grid, dim3(64), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
-    default: launch(attn_partial_kernel<8>, grid, dim3(64), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
+    case 2: launch(attn_partial_kernel<2>, grid, dim3(128), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
+    case 4: launch(attn_partial_kernel<4>, grid, dim3(256), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
+    default: launch(attn_partial_kernel<8>, grid, dim3(512), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
   }
-  launch(attn_combine_kernel, dim3((unsigned)Hq), dim3(kHeadDim), 0, stream, e2, (const float*)ws, T, out);
+  launch(attn_combine_kernel, dim3((unsigned)Hq), dim3(64), 0, stream, e2, (const float*)ws, T, out);
   return hipGetLastError();
 }
 
 hipError_t launch_silu_mul(const uint16_t* gu, uint16_t* y, int64_t M, int64_t I, hipStream_t stream,
                            const LaunchEvents& ev) {
-  const int64_t n = M * I;
-  launch(silu_mul_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, ev, gu, y, M, I);
+  launch(silu_mul_kernel, dim3((unsigned)((I + 255) / 256), (unsigned)M), dim3(256), 0, stream, ev, gu, y, I);
   return hipGetLastError();
 }
 

@@ -1,0 +1,86 @@
+"""One batch-1 decode step of a Qwen3-shaped decoder on the library's kernels.
+
+Each layer: residual add + RMSNorm, the fused q|k|v linear, per-head q/k
+RMSNorm + rotary embedding + KV-cache append, attention over the cache, the
+o linear, residual add + RMSNorm, the fused gate|up linear, SiLU-and-multiply,
+the down linear (whose output the next layer's first norm adds to the
+residual).  The step ends with the final norm; the LM head is not part of it.
+Argument marshalling only: every operation is a call of liblaq.so, except the
+linears, which the caller supplies (the library's quantized linear, or any
+other implementation of y = x W^T to compare against).
+"""
+import numpy as np
+
+from . import laq
+
+HEAD_DIM = laq.HEAD_DIM
+
+# Qwen3-4B decoder shape (hidden, query heads, key/value heads, MLP width).
+QWEN3_4B = {"layers": 36, "hidden": 2560, "heads": 32, "kv_heads": 8, "mlp": 9728,
+            "eps": 1e-6, "rope_theta": 1e6}
+
+
+def rope_table(S_max, theta, device, d=HEAD_DIM):
+    """fp32 [S_max][d]: cos of the d/2 rotation angles pos * theta^(-2i/d) of
+    each position, then their sin (angles and cos/sin in float64)."""
+    import torch
+    a = np.arange(S_max, dtype=np.float64)[:, None] * theta ** (-2.0 * np.arange(d // 2) / d)[None, :]
+    t = np.concatenate([np.cos(a), np.sin(a)], axis=1).astype(np.float32)
+    return torch.from_numpy(t).to(device)
+
+
+class DecodeStep:
+    """Buffers and call sequence of one decode step.
+
+    linears[l] = (qkv, o, gate_up, down): callables f(x, out) writing
+    out = x W^T (fp16 [1][N]) for the layer's weights.  norms[l] =
+    (input_norm, post_attention_norm, q_norm, k_norm) fp16 vectors;
+    final_norm fp16 [hidden].  k_caches / v_caches: fp16 [kv_heads][S_max][128]
+    per layer (positions below the decoded one already filled).
+    """
+
+    def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device):
+        import torch
+        self.s = shape
+        self.linears, self.norms, self.final_norm = linears, norms, final_norm
+        self.k_caches, self.v_caches = k_caches, v_caches
+        D, Hq, Hkv, I = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"]
+        S_max = k_caches[0].shape[1]
+        self.S_max = S_max
+        self.cos_sin = rope_table(S_max, shape["rope_theta"], device)
+        f16 = dict(dtype=torch.float16, device=device)
+        self.residual = torch.zeros((1, D), dtype=torch.float32, device=device)
+        self.x0 = torch.zeros((1, D), dtype=torch.float32, device=device)  # the token's embedding
+        self.h = torch.empty((1, D), **f16)
+        self.qkv = torch.empty((1, (Hq + 2 * Hkv) * HEAD_DIM), **f16)
+        self.q = torch.empty((Hq, HEAD_DIM), **f16)
+        self.attn = torch.empty((Hq, HEAD_DIM), **f16)
+        self.o = torch.empty((1, D), **f16)
+        self.gu = torch.empty((1, 2 * I), **f16)
+        self.m = torch.empty((1, I), **f16)
+        self.down = torch.empty((1, D), **f16)
+        self.out = torch.empty((1, D), **f16)
+        self.workspace = torch.empty(laq.attention_workspace_bytes(Hq, S_max), dtype=torch.uint8, device=device)
+
+    def run(self, pos):
+        """Decode the token at position pos (attends to positions 0..pos)."""
+        s = self.s
+        Hq, Hkv, eps = s["heads"], s["kv_heads"], s["eps"]
+        self.residual.copy_(self.x0)
+        delta = None
+        for l, (f_qkv, f_o, f_gu, f_down) in enumerate(self.linears):
+            w_in, w_post, qn, kn = self.norms[l]
+            laq.add_rmsnorm(self.residual, delta, w_in, eps, out=self.h)
+            f_qkv(self.h, self.qkv)
+            laq.qk_norm_rope(self.qkv, qn, kn, self.cos_sin, pos, Hq, Hkv, eps, self.k_caches[l], self.v_caches[l],
+                             q_out=self.q)
+            laq.decode_attention(self.q, self.k_caches[l], self.v_caches[l], pos + 1, out=self.attn,
+                                 workspace=self.workspace)
+            f_o(self.attn.view(1, Hq * HEAD_DIM), self.o)
+            laq.add_rmsnorm(self.residual, self.o, w_post, eps, out=self.h)
+            f_gu(self.h, self.gu)
+            laq.silu_mul(self.gu, out=self.m)
+            f_down(self.m, self.down)
+            delta = self.down
+        laq.add_rmsnorm(self.residual, delta, self.final_norm, eps, out=self.out)
+        return self.out

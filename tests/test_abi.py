@@ -253,5 +253,6 @@ def test_decode_ops_validation(L):
     assert f(None, ctypes.c_void_p(FAKE), 1, 8, None) == laq.LAQ_ERR_NULL_POINTER
     assert f(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 0, 8, None) == laq.LAQ_ERR_BAD_SHAPE
     assert f(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 1, 0, None) == laq.LAQ_ERR_BAD_SHAPE
+    assert f(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 65536, 8, None) == laq.LAQ_ERR_BAD_SHAPE
     assert f(ctypes.c_void_p(FAKE + 1), ctypes.c_void_p(FAKE), 1, 8, None) == laq.LAQ_ERR_MISALIGNED
     assert b"laq_silu_mul_f16" in L.laq_last_error()

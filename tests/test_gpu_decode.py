@@ -167,3 +167,44 @@ def test_decoder_layer_4b():
         r = linear_check(got, ref)
         assert r["ok"], (name, r)
     assert np.allclose(r_mid, r_ref, rtol=1e-6, atol=1e-5)
+
+
+def test_decode_step_graph_replay():
+    """paper_2605_08755_amd.decode.DecodeStep over two Qwen3-4B-shaped layers
+    with W3 linears: HIP-graph replays equal the eager step bitwise, and the
+    step equals the same calls issued one by one."""
+    say("decode step graph")
+    from paper_2605_08755_amd import decode
+    shape = dict(decode.QWEN3_4B, layers=2)
+    D, Hq, Hkv, I, S = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256
+    rng = np.random.default_rng(12)
+    lins, norms, kcs, vcs = [], [], [], []
+    for l in range(2):
+        fs = []
+        for j, (N, K) in enumerate((((Hq + 2 * Hkv) * 128, D), (D, Hq * 128), (2 * I, D), (D, I))):
+            q, s, z = laq.quantize(dev(inputs.weights(N, K, cfg=41, layer=l, proj=j)), 3)
+            fs.append(lambda x, out, q=q, s=s, z=z: laq.linear(x, q, s, z, 3, out=out))
+        lins.append(tuple(fs))
+        norms.append(tuple(dev((1 + 0.1 * rng.standard_normal(n)).astype(np.float16)) for n in (D, D, 128, 128)))
+        kcs.append(dev(f16(rng, (Hkv, S, 128))))
+        vcs.append(dev(f16(rng, (Hkv, S, 128))))
+    fin = dev((1 + 0.1 * rng.standard_normal(D)).astype(np.float16))
+    step = decode.DecodeStep(shape, lins, norms, fin, kcs, vcs, DEV)
+    step.x0.copy_(dev(rng.standard_normal((1, D)).astype(np.float32)))
+    pos = 200
+    eager = step.run(pos).clone()
+    torch.cuda.synchronize()
+    assert torch.isfinite(eager.float()).all()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        step.run(pos)
+    for _ in range(3):
+        step.out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(step.out.view(torch.int16), eager.view(torch.int16))
+        step.run(pos)  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(step.out.view(torch.int16), eager.view(torch.int16))
+    del g
