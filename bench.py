@@ -272,15 +272,30 @@ def decode_step_extra(stack, dev, steps, context=1024):
         w = stack.fp16[i]
         return lambda x, out: torch.mm(x, w.t(), out=out)
 
+    I = shape["mlp"]
+    swiglu_w = {}
+
+    def w3_swiglu_lin(i):
+        # gate|up rows interleaved (gate j, up j), quantized per row as before
+        if i % 4 != 2:
+            return w3_lin(i)
+        w = stack.fp16[i]
+        q, sc, z = swiglu_w[i] = laq.quantize(torch.stack([w[:I], w[I:]], dim=1).reshape(2 * I, -1).contiguous(), 3)
+        f = lambda x, out: laq.linear_swiglu(x, q, sc, z, 3, out=out)
+        f.swiglu = True
+        return f
+
     out = {"context": context, "layers": shape["layers"]}
-    for name, mk in (("w3", w3_lin), ("fp16", fp16_lin)):
+    for name, mk in (("w3", w3_lin), ("w3_fused_swiglu", w3_swiglu_lin), ("fp16", fp16_lin)):
         lins = [tuple(mk(4 * l + j) for j in range(4)) for l in range(shape["layers"])]
         step = decode.DecodeStep(shape, lins, norms, vec(D), [c[0] for c in caches], [c[1] for c in caches], dev)
         step.x0.copy_(torch.randn((1, D), generator=g, device=dev))
         ms, _ = time_graph(stack, 1, 3, steps, 5, step_fn=lambda: step.run(context - 1))
         out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}
         del step
+    swiglu_w.clear()
     out["w3_speedup_vs_fp16"] = round(out["fp16"]["us"] / out["w3"]["us"], 3)
+    out["w3_fused_swiglu_speedup_vs_fp16"] = round(out["fp16"]["us"] / out["w3_fused_swiglu"]["us"], 3)
     return out
 
 

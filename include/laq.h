@@ -206,6 +206,27 @@ laq_status laq_linear_ws_w3g128(const void *x, const uint32_t *qweight,
                                 void *stream);
 
 /*
+ * laq_linear_swiglu_w3g128 -- the gate|up projection of a SwiGLU MLP block
+ * with SiLU-and-multiply in its output stage (the decode step's MLP input,
+ * one launch instead of a linear and a separate elementwise kernel).  The
+ * weight rows come in pairs: row 2j is gate row j and row 2j + 1 is up row j
+ * (quantized as any other rows).  With a = sum_k x[m][k] s[2j][g] (q - z) and
+ * b the same sum over row 2j + 1, both in fp32,
+ *   y[m][j] = fp16(a / (1 + exp(-a)) * b),   j < N / 2
+ * rounded once (a and b are not rounded to fp16 first).
+ *
+ *   x        [in]  fp16 [M][K], 1 <= M <= 4
+ *   qweight, scales, zeros [in] as for laq_linear_w3g128, N rows, N even
+ *   y        [out] fp16 [M][N/2]
+ *   K        K <= 16384 / M' with M' = M rounded up to 1, 2 or 4 (the
+ *            activation tile stays in LDS); larger shapes: LAQ_ERR_BAD_SHAPE.
+ */
+laq_status laq_linear_swiglu_w3g128(const void *x, const uint32_t *qweight,
+                                    const void *scales, const uint8_t *zeros,
+                                    void *y, int64_t M, int64_t N, int64_t K,
+                                    void *stream);
+
+/*
  * laq_linear_group_w3g128 -- several independent laq_linear_w3g128 calls
  * (1 <= count <= LAQ_MAX_GROUP) with the same M, issued as one kernel launch:
  * for instance the q, k and v projections of a decoder layer, which read the
@@ -261,6 +282,11 @@ laq_status laq_linear_ws_w4g128(const void *x, const uint32_t *qweight,
                                 void *y, int64_t M, int64_t N, int64_t K,
                                 void *workspace, int64_t workspace_bytes,
                                 void *stream);
+
+laq_status laq_linear_swiglu_w4g128(const void *x, const uint32_t *qweight,
+                                    const void *scales, const uint8_t *zeros,
+                                    void *y, int64_t M, int64_t N, int64_t K,
+                                    void *stream);
 
 /* ------------------------------------------------------------------------
  * Decode-step operations around the linears of a decoder layer (the model

@@ -306,6 +306,43 @@ laq_status laq_decode_attention_f16(const void* q, const void* k_cache, const vo
                             static_cast<float*>(workspace), static_cast<hipStream_t>(stream), ev));
 }
 
+}  // extern "C"
+
+namespace {
+
+template <int BITS>
+laq_status linear_swiglu(const char* fn, const void* x, const uint32_t* qweight, const void* scales,
+                         const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {
+  const laq::LaunchEvents ev = take_events();
+  if (!x || !qweight || !scales || !zeros || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (M < 1 || M > 4) return fail(LAQ_ERR_BAD_M, fn, "M must be in 1..4");
+  if (N % 2 != 0) return fail(LAQ_ERR_BAD_SHAPE, fn, "N (gate and up rows interleaved) must be even");
+  if (!laq::swiglu_fits((int)M, K))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need K <= 16384 / M' (M' = M rounded up to 1, 2 or 4)");
+  if (!aligned(x, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "x and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  return hip_status(fn, laq::launch_linear_swiglu<BITS>(static_cast<const uint16_t*>(x), qweight,
+                                                        static_cast<const uint16_t*>(scales), zeros,
+                                                        static_cast<uint16_t*>(y), (int)M, N, K,
+                                                        static_cast<hipStream_t>(stream), ev));
+}
+
+}  // namespace
+
+extern "C" {
+
+laq_status laq_linear_swiglu_w3g128(const void* x, const uint32_t* qweight, const void* scales,
+                                    const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {
+  return linear_swiglu<3>("laq_linear_swiglu_w3g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+laq_status laq_linear_swiglu_w4g128(const void* x, const uint32_t* qweight, const void* scales,
+                                    const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {
+  return linear_swiglu<4>("laq_linear_swiglu_w4g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
 laq_status laq_silu_mul_f16(const void* gate_up, void* y, int64_t M, int64_t I, void* stream) {
   const char* fn = "laq_silu_mul_f16";
   const laq::LaunchEvents ev = take_events();

@@ -129,6 +129,14 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
                          hipStream_t stream, const LaunchEvents& ev, float* workspace = nullptr,
                          size_t workspace_bytes = 0);
 
+// Gate|up linear with SiLU-and-multiply in its output stage: weight rows in
+// (gate, up) pairs, y fp16 [M][N/2].  Shapes: swiglu_fits(M, K), N even.
+bool swiglu_fits(int M, int64_t K);
+template <int BITS>
+hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
+                                const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K, hipStream_t stream,
+                                const LaunchEvents& ev);
+
 // Decode-step operations (decode.hip); head dimension 128.
 int64_t decode_attention_tiles(int64_t L);
 hipError_t launch_add_rmsnorm(float* res, const uint16_t* delta, const uint16_t* w, uint16_t* y, int64_t M,

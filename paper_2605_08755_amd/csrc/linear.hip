@@ -303,10 +303,35 @@ __device__ __forceinline__ void units_dot(const u32x4 (&wv)[RPL][BITS], const u3
   }
 }
 
+// Output stage of the fused gate|up + SiLU-and-multiply linear: the weight
+// rows come in (gate, up) pairs, rows 2j and 2j + 1, and output column
+// (row0 + 2j) / 2 of the N / 2 columns is silu(gate) * up of the two rows'
+// fp32 sums, rounded once to fp16.  R, row0 and rows are even.
+template <int MT, int NT>
+__device__ __forceinline__ void swiglu_rows(const float* part, int R, int G, int rows, int M, int N, int64_t row0,
+                                            uint16_t* __restrict__ y, int t) {
+  const int l = t & 15;
+  for (int pr = t >> 4; 2 * pr < rows; pr += NT / 16) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      float ag = 0.0f, au = 0.0f;
+      for (int g = l; g < G; g += 16) {
+        ag += part[m * R * G + (2 * pr) * G + g];
+        au += part[m * R * G + (2 * pr + 1) * G + g];
+      }
+      ag = row16_sum(ag);
+      au = row16_sum(au);
+      if (l == 0 && m < M)
+        y[(int64_t)m * (N / 2) + row0 / 2 + pr] = __builtin_bit_cast(uint16_t, (_Float16)(ag / (1.0f + expf(-ag)) * au));
+    }
+  }
+}
+
 // One block of the flat kernel: rows block*R .. block*R + R - 1 of one call.
 // Thread t takes units t + i*NT (i < UPT) of each pass over the block's
 // units; every launch uses UPT = 1 (more units per thread measured slower).
-template <int BITS, int MT, int NT, int UPT, int XB>
+// SW: the fused gate|up + SiLU-and-multiply output stage (swiglu_rows).
+template <int BITS, int MT, int NT, int UPT, int XB, bool SW = false>
 __device__ __forceinline__ void flat_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
@@ -438,13 +463,17 @@ __device__ __forceinline__ void flat_block(
 
   // 5. Row sums in a fixed order: lane l of a row's 16 adds groups l, l+16, ...
   const int l = t & 15;
-  for (int rr = t >> 4; rr < rows; rr += NT / 16) {
+  if constexpr (SW) {
+    swiglu_rows<MT, NT>(part, R, G, rows, M, N, row0, y, t);
+  } else {
+    for (int rr = t >> 4; rr < rows; rr += NT / 16) {
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      float acc = 0.0f;
-      for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
-      acc = row16_sum(acc);
-      if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+      for (int m = 0; m < MT; ++m) {
+        float acc = 0.0f;
+        for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
+        acc = row16_sum(acc);
+        if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+      }
     }
   }
 }
@@ -453,7 +482,7 @@ __device__ __forceinline__ void flat_block(
 // form RPL layers of R1 = R / RPL rows (R1 * G <= NT), and thread
 // t = r*G + g of the first layer takes group g of rows r, r + R1, r + 2*R1,
 // ...  Loads, staging and the row sums are those of flat_block.
-template <int BITS, int MT, int NT, int RPL, int XB>
+template <int BITS, int MT, int NT, int RPL, int XB, bool SW = false>
 __device__ __forceinline__ void flat_block_rpl(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
@@ -528,18 +557,22 @@ __device__ __forceinline__ void flat_block_rpl(
 
   // 4. Row sums in a fixed order: lane l of a row's 16 adds groups l, l+16, ...
   const int l = t & 15;
-  for (int rr = t >> 4; rr < rows; rr += NT / 16) {
+  if constexpr (SW) {
+    swiglu_rows<MT, NT>(part, R, G, rows, M, N, row0, y, t);
+  } else {
+    for (int rr = t >> 4; rr < rows; rr += NT / 16) {
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      float acc = 0.0f;
-      for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
-      acc = row16_sum(acc);
-      if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+      for (int m = 0; m < MT; ++m) {
+        float acc = 0.0f;
+        for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
+        acc = row16_sum(acc);
+        if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+      }
     }
   }
 }
 
-template <int BITS, int MT, int NT, int RPL, int XB>
+template <int BITS, int MT, int NT, int RPL, int XB, bool SW>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
@@ -548,9 +581,9 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
   // early return: the argument loads then go out as one batch).
   (void)nblocks;
   if constexpr (RPL == 1)
-    flat_block<BITS, MT, NT, 1, XB>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+    flat_block<BITS, MT, NT, 1, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
   else
-    flat_block_rpl<BITS, MT, NT, RPL, XB>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+    flat_block_rpl<BITS, MT, NT, RPL, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
 }
 
 // Several independent calls in one launch: block b belongs to the last call
@@ -647,9 +680,9 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
       const unsigned blocks = xcd_grid(nblocks);
       tune.last_blocks = nblocks;
       tune.last_rows = R;
-#define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                        \
-  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
-         qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+#define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                     \
+  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
+         ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
 #define LAQ_FLAT_NT(MTV, XBV, NTV)                       \
   do {                                                   \
     if (RPL == 2) LAQ_FLAT_K(MTV, XBV, NTV, 2);          \
@@ -708,6 +741,48 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     default: LAQ_LAUNCH(16); break;
   }
 #undef LAQ_LAUNCH
+  return hipGetLastError();
+}
+
+bool swiglu_fits(int M, int64_t K) { return M >= 1 && M <= 4 && K >= 128 && K % 128 == 0 && ceil_pow2(M) * K <= 16384; }
+
+template <int BITS>
+hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
+                                const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K, hipStream_t stream,
+                                const LaunchEvents& ev) {
+  // The flat kernel at one row per lane with an even number of rows per
+  // block, so that every (gate, up) pair of rows meets in one block's
+  // partials.  MT * G <= 128 keeps the activation tile and the partials
+  // within 52 KB of LDS.
+  if (!swiglu_fits(M, K) || N % 2 != 0) return hipErrorInvalidValue;
+  const int G = (int)(K / 128);
+  const int MT = ceil_pow2(M);
+  const int NT = G <= 32 ? 256 : G <= 64 ? 512 : (MT == 1 ? 256 : 512);
+  const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
+  int R = max(1, min(NT / G, 4096 / (G * MT)));
+  R = max(2, R & ~1);
+  const size_t lds = (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * R * G * 4;
+  const int nblocks = (int)((N + R - 1) / R);
+  const unsigned blocks = xcd_grid(nblocks);
+#define LAQ_SW_K(MTV, XBV, NTV)                                                                                   \
+  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV, true>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
+         qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+#define LAQ_SW_NT(MTV, XBV)                 \
+  do {                                      \
+    if (NT == 512) LAQ_SW_K(MTV, XBV, 512); \
+    else LAQ_SW_K(MTV, XBV, 256);           \
+  } while (0)
+#define LAQ_SW_XB(MTV)              \
+  if (XB == 2) LAQ_SW_NT(MTV, 2);   \
+  else LAQ_SW_NT(MTV, 5);
+  switch (MT) {
+    case 1: LAQ_SW_XB(1); break;
+    case 2: LAQ_SW_XB(2); break;
+    default: LAQ_SW_XB(4); break;
+  }
+#undef LAQ_SW_XB
+#undef LAQ_SW_NT
+#undef LAQ_SW_K
   return hipGetLastError();
 }
 
@@ -772,6 +847,10 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
   return hipGetLastError();
 }
 
+template hipError_t launch_linear_swiglu<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
+                                            uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
+template hipError_t launch_linear_swiglu<4>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
+                                            uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_group<3>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,

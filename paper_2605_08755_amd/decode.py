@@ -33,7 +33,9 @@ class DecodeStep:
     """Buffers and call sequence of one decode step.
 
     linears[l] = (qkv, o, gate_up, down): callables f(x, out) writing
-    out = x W^T (fp16 [1][N]) for the layer's weights.  norms[l] =
+    out = x W^T (fp16 [1][N]) for the layer's weights; a gate_up callable
+    with the attribute swiglu = True writes silu(gate) * up (fp16 [1][I])
+    itself (laq.linear_swiglu), and the step skips silu_mul.  norms[l] =
     (input_norm, post_attention_norm, q_norm, k_norm) fp16 vectors;
     final_norm fp16 [hidden].  k_caches / v_caches: fp16 [kv_heads][S_max][128]
     per layer (positions below the decoded one already filled).
@@ -78,8 +80,11 @@ class DecodeStep:
                                  workspace=self.workspace)
             f_o(self.attn.view(1, Hq * HEAD_DIM), self.o)
             laq.add_rmsnorm(self.residual, self.o, w_post, eps, out=self.h)
-            f_gu(self.h, self.gu)
-            laq.silu_mul(self.gu, out=self.m)
+            if getattr(f_gu, "swiglu", False):
+                f_gu(self.h, self.m)
+            else:
+                f_gu(self.h, self.gu)
+                laq.silu_mul(self.gu, out=self.m)
             f_down(self.m, self.down)
             delta = self.down
         laq.add_rmsnorm(self.residual, delta, self.final_norm, eps, out=self.out)

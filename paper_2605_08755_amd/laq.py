@@ -27,7 +27,8 @@ EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profil
            "laq_quantize_w4g128", "laq_pack_w4g128", "laq_linear_w4g128", "laq_linear_group_w4g128",
            "laq_linear_workspace_bytes", "laq_linear_ws_w3g128", "laq_linear_ws_w4g128",
            "laq_add_rmsnorm_f16", "laq_qk_norm_rope_f16", "laq_decode_attention_workspace_bytes",
-           "laq_decode_attention_f16", "laq_silu_mul_f16")
+           "laq_decode_attention_f16", "laq_silu_mul_f16", "laq_linear_swiglu_w3g128",
+           "laq_linear_swiglu_w4g128")
 HEAD_DIM = 128
 
 
@@ -74,7 +75,8 @@ def lib():
             f = getattr(L, name)
             f.argtypes = [ctypes.POINTER(LinearCall), ctypes.c_int32, I64, P]
             f.restype = ctypes.c_int32
-        for name in ("laq_linear_w3g128", "laq_linear_w4g128"):
+        for name in ("laq_linear_w3g128", "laq_linear_w4g128", "laq_linear_swiglu_w3g128",
+                     "laq_linear_swiglu_w4g128"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, P, P, I64, I64, I64, P]
             f.restype = ctypes.c_int32
@@ -189,6 +191,23 @@ def linear(x, qweight, scales, zeros, bits=3, out=None, split_k=True):
                   _stream(x.device)))
         return y
     fn = lib().laq_linear_w3g128 if bits == 3 else lib().laq_linear_w4g128
+    _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _stream(x.device)))
+    return y
+
+
+def linear_swiglu(x, qweight, scales, zeros, bits=3, out=None):
+    """silu(gate) * up of the gate|up projection in one launch: fp16 x [M][K]
+    (M <= 4) against packed weights whose rows alternate gate row j, up row j
+    (N = 2 I rows); returns fp16 [M][I]."""
+    import torch
+    assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+    M, K = x.shape
+    N = scales.shape[0]
+    assert qweight.numel() == packed_words(bits, N, K) and qweight.is_contiguous()
+    assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+    assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+    y = torch.empty((M, N // 2), dtype=torch.float16, device=x.device) if out is None else out
+    fn = lib().laq_linear_swiglu_w3g128 if bits == 3 else lib().laq_linear_swiglu_w4g128
     _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _stream(x.device)))
     return y
 

@@ -90,6 +90,28 @@ def test_pack_validation(L, bits):
     assert b"laq_pack" in L.laq_last_error()
 
 
+def _sw(L, bits, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, M=1, N=4, K=128):
+    f = L.laq_linear_swiglu_w3g128 if bits == 3 else L.laq_linear_swiglu_w4g128
+    return f(ctypes.c_void_p(x), ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z),
+             ctypes.c_void_p(y), M, N, K, None)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_swiglu_validation(L, bits):
+    for kw in ("x", "q", "s", "z", "y"):
+        assert _sw(L, bits, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _sw(L, bits, M=0) == laq.LAQ_ERR_BAD_M
+    assert _sw(L, bits, M=5) == laq.LAQ_ERR_BAD_M
+    assert _sw(L, bits, N=3) == laq.LAQ_ERR_BAD_SHAPE     # rows come in (gate, up) pairs
+    assert _sw(L, bits, K=127) == laq.LAQ_ERR_BAD_SHAPE
+    assert _sw(L, bits, K=16384 + 128) == laq.LAQ_ERR_BAD_SHAPE
+    assert _sw(L, bits, M=2, K=8192 + 128) == laq.LAQ_ERR_BAD_SHAPE
+    assert _sw(L, bits, M=3, K=4096 + 128) == laq.LAQ_ERR_BAD_SHAPE
+    assert _sw(L, bits, x=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert _sw(L, bits, y=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_linear_swiglu" in L.laq_last_error()
+
+
 @pytest.mark.parametrize("bits", [3, 4])
 def test_linear_validation(L, bits):
     for kw in ("x", "q", "s", "z", "y"):

@@ -104,6 +104,25 @@ def test_silu_mul(M, I):
     assert r["ok"], r
 
 
+@pytest.mark.parametrize("M,I,K,bits", [(1, 9728, 2560, 3), (2, 100, 1024, 3), (3, 53, 4096, 4), (1, 37, 16384, 3),
+                                         (4, 64, 128, 3), (1, 1, 640, 4)])
+def test_linear_swiglu(M, I, K, bits):
+    """Gate|up linear with SiLU-and-multiply in its output stage against the
+    oracle's linear (fp64, unrounded) followed by its silu_mul, on weight rows
+    interleaved gate j, up j."""
+    say("linear_swiglu", M, I, K, bits)
+    w = inputs.weights(2 * I, K, cfg=41, proj=bits)
+    x = inputs.activations(M, K, cfg=41)
+    codes, s, z = oracle.quantize(w, bits)
+    y = laq.linear_swiglu(dev(x), dev(oracle.pack(codes, bits).view(np.int32)), dev(s.view(np.float16)), dev(z),
+                          bits)
+    torch.cuda.synchronize()
+    full = np.asarray(oracle.linear(x, codes, s, z), dtype=np.float64)
+    ref = OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I)
+    r = linear_check(y.cpu().numpy(), ref)
+    assert r["ok"], r
+
+
 def test_decoder_layer_4b():
     """One Qwen3-4B-shaped decoder layer at position pos = 300 with a filled
     cache: W3 linears and the decode operations on the GPU, against the oracle's
@@ -208,3 +227,47 @@ def test_decode_step_graph_replay():
         torch.cuda.synchronize()
         assert torch.equal(step.out.view(torch.int16), eager.view(torch.int16))
     del g
+
+
+def test_decode_step_fused_swiglu():
+    """DecodeStep with the gate|up linear that applies SiLU-and-multiply in its
+    output stage (weight rows interleaved gate j, up j) against the same step
+    with the plain gate|up linear followed by silu_mul, over two Qwen3-4B-shaped
+    layers.  The fused call skips the fp16 rounding of gate and up, so the two
+    agree to the fp16 precision of the step, not bitwise."""
+    say("decode step fused swiglu")
+    from paper_2605_08755_amd import decode
+    shape = dict(decode.QWEN3_4B, layers=2)
+    D, Hq, Hkv, I, S = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256
+    rng = np.random.default_rng(13)
+    plain, fused, norms, kcs, vcs = [], [], [], [], []
+    for l in range(2):
+        fs, ff = [], []
+        for j, (N, K) in enumerate((((Hq + 2 * Hkv) * 128, D), (D, Hq * 128), (2 * I, D), (D, I))):
+            w = dev(inputs.weights(N, K, cfg=42, layer=l, proj=j))
+            q, s, z = laq.quantize(w, 3)
+            fs.append(lambda x, out, q=q, s=s, z=z: laq.linear(x, q, s, z, 3, out=out))
+            if j == 2:
+                qi, si, zi = laq.quantize(torch.stack([w[:I], w[I:]], dim=1).reshape(N, K).contiguous(), 3)
+                f = lambda x, out, q=qi, s=si, z=zi: laq.linear_swiglu(x, q, s, z, 3, out=out)
+                f.swiglu = True
+                ff.append(f)
+            else:
+                ff.append(fs[-1])
+        plain.append(tuple(fs))
+        fused.append(tuple(ff))
+        norms.append(tuple(dev((1 + 0.1 * rng.standard_normal(n)).astype(np.float16)) for n in (D, D, 128, 128)))
+        kcs.append(f16(rng, (Hkv, S, 128)))
+        vcs.append(f16(rng, (Hkv, S, 128)))
+    fin = dev((1 + 0.1 * rng.standard_normal(D)).astype(np.float16))
+    x0 = dev(rng.standard_normal((1, D)).astype(np.float32))
+    outs = []
+    for lins in (plain, fused):
+        step = decode.DecodeStep(shape, lins, norms, fin, [dev(a) for a in kcs], [dev(a) for a in vcs], DEV)
+        step.x0.copy_(x0)
+        outs.append(step.run(200).float().cpu().numpy())
+        torch.cuda.synchronize()
+    a, b = outs
+    assert np.isfinite(b).all()
+    rms = float(np.sqrt(np.mean(a ** 2)))
+    assert float(np.abs(a - b).max()) <= 1e-2 * rms, (float(np.abs(a - b).max()), rms)
