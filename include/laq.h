@@ -10,13 +10,13 @@
  *
  *   laq_quantize_w3g128 -- Eq. 1 (Sec. 2): q = clip(round(w/s) + z, 0, 7)
  *                          with round-to-nearest min-max s, z per 128-group,
- *                          packed 32 codes per three 32-bit words (App. G).
+ *                          packed 32 codes per three 32-bit words (App. H).
  *   laq_pack_w3g128     -- Eq. 1 with caller-supplied s, z (for instance the
  *                          scale and zero point LAQuant's QAT learned),
  *                          packed the same way.
  *   laq_linear_w3g128   -- y = x * w_hat^T with w_hat = s * (q - z) (Eq. 1),
  *                          the fused dequantize GEMV / skinny GEMM of decode
- *                          (App. G describes the paper's INT3 GEMV).
+ *                          (App. H describes the paper's INT3 GEMV).
  *
  * plus the W4G128 (4-bit, 8 codes per word) siblings used for bit-width
  * comparison (Table 3 reports W4G128 and W3G128 decoding).
@@ -169,7 +169,7 @@ laq_status laq_linear_w3g128(const void *x, const uint32_t *qweight,
  * laq_linear_workspace_bytes -- device workspace (bytes) with which
  * laq_linear_ws_w3g128 / laq_linear_ws_w4g128 split K across workgroups for
  * an (M, N, K) call: the reduction along K of Eq. 1's dot products, which
- * App. G's GEMV spreads over a 2-D grid of thread blocks, here deterministic
+ * App. H's GEMV spreads over a 2-D grid of thread blocks, here deterministic
  * (fp32 partial sums per K range, added in a fixed order by a second kernel).
  * It applies on the matrix-core path (M >= 2) to rows of at least 40 quads
  * of four groups (K > 19968) and fewer than 1024 tiles of 16 rows

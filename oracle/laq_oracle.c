@@ -20,7 +20,7 @@
  *    contain 0 (lo <= 0 <= hi).  Arithmetic: IEEE fp32, round-half-to-even,
  *    true division, the scale rounded to fp16 before it is used.  The codes
  *    of Eq. 1 for caller-supplied (e.g. trained) s and z are computed too.
- *  - Packing: 32 three-bit codes in three 32-bit words (App. G keeps this
+ *  - Packing: 32 three-bit codes in three 32-bit words (App. H keeps this
  *    density of the GPTQ INT3 kernel), in this library's bit order; 4-bit
  *    codes eight per word.  The bit positions are computed here from the
  *    written definition, one code at a time.

@@ -47,21 +47,13 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
     hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
 }
 
-// Launch-shape parameters of the GEMV (defaults tuned on MI355X; exposed
-// internally so measurement harnesses can sweep them).
-struct LinearTuning {
-  int flat_threads = 0;      // flat kernel: threads per block (64 .. 1024); 0 = chosen from the shape
-  int flat_rpl = 0;          // flat kernel: rows per lane (1 or 2); 0 = chosen from the shape
-  int flat_resident_waves = 8192;  // waves the chip keeps resident (256 compute units x 32)
-  int last_blocks = 0;       // launch shape of the most recent flat launch (for harnesses)
-  int last_rows = 0;
-  int mfma_min_m = 3;        // activation rows from which the matrix-core path may be used
-  int mfma_waves = 0;        // matrix-core kernel: waves per block (1..16); 0 = one per group quad
-  int mfma_tiles = 0;        // matrix-core kernel: 16-row tiles per block (1 or 2); 0 = chosen from N
-  int mfma_share_min_tiles = 1024;  // from this many 16-row tiles: four tiles per block share the activations
-  int split_min_quads = 40;         // fewer tiles: K is split (given a workspace) from rows of this many quads
-};
-LinearTuning& linear_tuning();
+// Routing constants of the linear (measured on MI355X).  Every launch shape
+// is a pure function of (M, N, K) and these constants: the library keeps no
+// mutable state between calls.
+constexpr int kMfmaMinM = 3;               // activation rows from which the matrix-core path may be used
+constexpr int kResidentWaves = 8192;       // waves the chip keeps resident (256 compute units x 32)
+constexpr int kMfmaShareMinTiles = 1024;   // from this many 16-row tiles: tiles per block share the activations
+constexpr int kSplitMinQuads = 40;         // fewer tiles: K is split (given a workspace) from rows of this many quads
 
 // Several independent linears in one launch (kernel argument block, by value).
 constexpr int kMaxGroup = 8;
@@ -92,10 +84,10 @@ template <int BITS>
 hipError_t launch_pack(const uint16_t* w, const uint16_t* scales, const uint8_t* zeros, int64_t N,
                        int64_t K, uint32_t* qweight, hipStream_t stream, const LaunchEvents& ev);
 
-// Split K on the matrix-core path for fewer than mfma_share_min_tiles row
-// tiles and rows of at least split_min_quads quads: S K ranges of qs quads,
+// Split K on the matrix-core path for fewer than kMfmaShareMinTiles row
+// tiles and rows of at least kSplitMinQuads quads: S K ranges of qs quads,
 // tile_blocks blocks of four tiles per range; S == 1 means no split.  A pure
-// function of the shape (and the tuning).
+// function of the shape.
 struct SplitPlan {
   int S = 1;
   int qs = 0;

@@ -609,11 +609,6 @@ int ceil_pow2(int v) {
 
 }  // namespace
 
-LinearTuning& linear_tuning() {
-  static LinearTuning t;
-  return t;
-}
-
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
@@ -624,7 +619,7 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   // Matrix cores from mfma_min_m rows on, except that the VALU kernel stays
   // ahead up to 4 rows when rows are short (measured on MI355X: it re-reads
   // the activations from LDS per unit, which costs more as rows get longer).
-  if (M >= linear_tuning().mfma_min_m && !(M <= 4 && G <= 24))
+  if (M >= kMfmaMinM && !(M <= 4 && G <= 24))
     return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev, workspace, workspace_bytes);
   const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
@@ -633,16 +628,14 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     // One (row, group) unit per thread (fewest loads per lane measured best on
     // every shape) and whole rows per block, so the reduction stays inside
     // the block.
-    LinearTuning& tune = linear_tuning();
     // Threads per block: every block stages the whole activation row, so
     // longer rows want more rows per block (about 8 or more) to amortize it;
     // short rows with few of them use smaller blocks so that the grid still
     // covers the compute units.
     // Rows of 65..128 groups use 256 threads at one activation row and 512
     // at two, with two rows per lane (below).
-    int NT = tune.flat_threads;
-    if (NT == 0) NT = G <= 32 ? 256 : G <= 64 ? 512 : G <= 128 ? (MT == 1 ? 256 : 512) : 1024;
-    if (tune.flat_threads == 0 && MT == 1)
+    int NT = G <= 32 ? 256 : G <= 64 ? 512 : G <= 128 ? (MT == 1 ? 256 : 512) : 1024;
+    if (MT == 1)
       while (NT > 64 && G <= 16 && NT / 2 >= G && (N + NT / G - 1) / (NT / G) < 256) NT /= 2;
     const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
     auto lds_bytes = [&](int rows) { return (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * rows * G * 4; };
@@ -658,11 +651,11 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     //  - two activation rows meet rows of 32..128 groups (twice the LDS
     //    reads per unit);
     // elsewhere one row per lane is faster (the lanes' own latency decides).
-    int want = tune.flat_rpl;
-    if (want == 0) {
+    int want;
+    {
       const int64_t waves1 = (N + R - 1) / R * (NT / 64);
       if (MT == 1)
-        want = (G > 64 && G <= 128) || (G <= 64 && waves1 > tune.flat_resident_waves) ? 2 : 1;
+        want = (G > 64 && G <= 128) || (G <= 64 && waves1 > kResidentWaves) ? 2 : 1;
       else
         want = (MT == 2 && G >= 32 && G <= 128) ? 2 : 1;
     }
@@ -678,8 +671,6 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
     if (MT <= 4 && lds <= 64 * 1024) {
       const int nblocks = (int)((N + R - 1) / R);
       const unsigned blocks = xcd_grid(nblocks);
-      tune.last_blocks = nblocks;
-      tune.last_rows = R;
 #define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                     \
   launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
          ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
@@ -792,7 +783,7 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
   for (int i = 0; i < count; ++i) G_max = max(G_max, calls[i].G);
   const int MT = ceil_pow2(M);
   // Same routing as a single call, decided on the longest row of the group.
-  if (M >= linear_tuning().mfma_min_m && !(M <= 4 && G_max <= 24))
+  if (M >= kMfmaMinM && !(M <= 4 && G_max <= 24))
     return launch_linear_mfma_group<BITS>(calls, count, M, stream, ev);
   const int NT = G_max <= 32 ? 256 : (G_max <= 64 ? 512 : 1024);
   const int XB = (MT * G_max * 16 <= 2 * NT) ? 2 : 5;

@@ -720,10 +720,9 @@ __global__ __launch_bounds__(1024) void linear_mfma_group_kernel(const LinearGro
 
 SplitPlan mfma_split_plan(int M, int64_t N, int G) {
   SplitPlan p;
-  const LinearTuning& tune = linear_tuning();
   const int64_t tiles = (N + 15) / 16;
   const int nq = (G + 3) / 4;
-  if (M < 2 || tune.mfma_tiles != 0 || tiles >= tune.mfma_share_min_tiles || nq < tune.split_min_quads) return p;
+  if (M < 2 || tiles >= kMfmaShareMinTiles || nq < kSplitMinQuads) return p;
   // Blocks of four tiles over K ranges of qs quads: the longest ranges (the
   // fewest partial sums) that still give every compute unit a block.
   const int64_t tile_blocks = (tiles + kFullTiles - 1) / kFullTiles;
@@ -740,7 +739,6 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
                               hipStream_t stream, const LaunchEvents& ev, float* workspace,
                               size_t workspace_bytes) {
   const int G = (int)(K / 128);
-  LinearTuning& tune = linear_tuning();
   const int nq = (G + 3) / 4;
   // Two tiles per block share each activation fragment when rows are long
   // (the fragments then outweigh the weights) and there are enough tiles to
@@ -750,10 +748,8 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   // Blocks of four tiles fit three to a compute unit (LDS), so up to 768
   // blocks are resident at once; from 3072 tiles on, blocks of eight (two to a
   // compute unit).
-  if (tune.mfma_tiles == 0 && tiles >= tune.mfma_share_min_tiles && nq <= 5) {
+  if (tiles >= kMfmaShareMinTiles && nq <= 5) {
     const int nblocks = (int)((tiles + kFullTiles - 1) / kFullTiles);
-    tune.last_blocks = nblocks;
-    tune.last_rows = 16 * kFullTiles;
     const dim3 grid(xcd_grid(nblocks)), blk(64 * kFullTiles);
     const uint32_t lds = (uint32_t)nq * kSlabBytes;
     switch (nq) {
@@ -765,11 +761,9 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
     }
     return hipGetLastError();
   }
-  if (tune.mfma_tiles == 0 && tiles >= tune.mfma_share_min_tiles) {
+  if (tiles >= kMfmaShareMinTiles) {
     const int tb = tiles >= 3072 ? 8 : 4;
     const int nblocks = (int)((tiles + tb - 1) / tb);
-    tune.last_blocks = nblocks;
-    tune.last_rows = 16 * tb;
     if (tb == 8)
       launch(linear_mfma_tiles_kernel<BITS, 8>, dim3(xcd_grid(nblocks)), dim3(512), kSlabLdsBytes, stream, ev, x,
              qweight, scales, zeros, y, M, (int)N, G, nblocks);
@@ -784,8 +778,6 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   const SplitPlan sp = mfma_split_plan(M, N, G);
   if (sp.S > 1 && workspace && workspace_bytes >= split_workspace_bytes(sp, M, N)) {
     const int nblocks = sp.tile_blocks * sp.S;
-    tune.last_blocks = nblocks;
-    tune.last_rows = 16 * kFullTiles;
     LaunchEvents e1, e2;  // the measurement hook spans both kernels
     e1.start = ev.start;
     e2.stop = ev.stop;
@@ -804,17 +796,15 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
     return hipGetLastError();
   }
   // (At most M tiles per wave: a wave's TW KiB of partials reuse its M KiB slab.)
-  const int TW = min(M, tune.mfma_tiles > 0 ? (tune.mfma_tiles >= 2 ? 2 : 1) : ((tiles >= 256 && G >= 32) ? 2 : 1));
+  const int TW = min(M, (tiles >= 256 && G >= 32) ? 2 : 1);
   // One wave per quad of the row, at most 8 (more waves per block measured
   // slower: Qwen3-4B down, 19 quads, at M = 16 10.3 us with 10 waves, 10.0
   // with 8) and as many M-row activation slabs (M KiB each) as fit in
   // 160 KiB; longer rows loop.
   const int wmax = min(8, kBlockLdsU4 / (M * kSlabRowU4));
-  const int W = tune.mfma_waves > 0 ? min(wmax, tune.mfma_waves) : min(wmax, nq);
+  const int W = min(wmax, nq);
   const int nblocks = (int)((tiles + TW - 1) / TW);
   const unsigned blocks = xcd_grid(nblocks);
-  tune.last_blocks = nblocks;
-  tune.last_rows = 16 * TW;
   const uint32_t lds = (uint32_t)W * M * kSlabRowU4 * 16;
   if (TW == 2)
     launch(linear_mfma_kernel<BITS, 2>, dim3(blocks), dim3(64 * W), lds, stream, ev, x, qweight, scales, zeros, y, M,

@@ -1,7 +1,7 @@
 // Quantize + pack kernel: Eq. 1 (Sec. 2) with round-to-nearest min-max
 // scale and zero point per group of 128 consecutive weights of a row, packed
 // into the plane layout of include/laq.h (32 codes in three 32-bit words for
-// W3, as App. G keeps; eight 4-bit codes per word for W4).
+// W3, as App. H keeps; eight 4-bit codes per word for W4).
 //
 // Mapping: a wave takes 16 consecutive groups (4 KiB of fp16, read as four
 // fully coalesced 1 KiB direct-to-LDS loads) and 4 lanes per group (a

@@ -406,7 +406,7 @@ def pin_pack_fields(o, seed=1):
 
 
 def pin_density(o, golden):
-    """App. G: 32 three-bit weights in three 32-bit words; BLOCKHEIGHT =
+    """App. H: 32 three-bit weights in three 32-bit words; BLOCKHEIGHT =
     BLOCKWIDTH/32*3 packed rows per BLOCKWIDTH inputs; group size 128."""
     codes = np.zeros((3, golden["group_size"]), np.uint8)
     qw = o.pack(codes, 3)
