@@ -206,6 +206,30 @@ laq_status laq_linear_ws_w3g128(const void *x, const uint32_t *qweight,
                                 void *stream);
 
 /*
+ * laq_linear_noalloc_w3g128 -- for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): laq_linear_ws_w3g128 with the split-K partial sums in a
+ * scratch array the library itself holds on each GPU, instead of a caller's
+ * workspace.  The call allocates nothing.
+ *
+ *   Arguments, layouts and results as for laq_linear_w3g128; the results
+ *   equal laq_linear_ws_w3g128's with a large enough workspace, bit for bit.
+ *   Scratch: LAQ_NOALLOC_SCRATCH_BYTES (8 MiB) per GPU, held from the first
+ *   call on that GPU until the process ends.  A shape whose partial sums
+ *   (laq_linear_workspace_bytes(M, N, K)) exceed it is rejected with
+ *   LAQ_ERR_BAD_SHAPE before anything is enqueued.  Every call on a GPU
+ *   shares that GPU's array: calls that may overlap in time on one GPU (on
+ *   different streams, or from several host threads) race on it and must be
+ *   ordered by the caller; the partial sums are fully written before they
+ *   are read, so nothing needs clearing between calls.
+ */
+#define LAQ_NOALLOC_SCRATCH_BYTES (8 << 20)
+laq_status laq_linear_noalloc_w3g128(const void *x, const uint32_t *qweight,
+                                     const void *scales, const uint8_t *zeros,
+                                     void *y, int64_t M, int64_t N, int64_t K,
+                                     void *stream);
+
+/*
  * laq_linear_swiglu_w3g128 -- the gate|up projection of a SwiGLU MLP block
  * with SiLU-and-multiply in its output stage (the decode step's MLP input,
  * one launch instead of a linear and a separate elementwise kernel).  The

@@ -1,9 +1,11 @@
 // C ABI of the library (include/laq.h): argument validation on the host,
 // then an asynchronous launch on the caller's stream.  Nothing is enqueued
 // when validation fails.
+#include <atomic>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "laq.h"
@@ -355,3 +357,80 @@ laq_status laq_silu_mul_f16(const void* gate_up, void* y, int64_t M, int64_t I, 
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// The linear without a caller workspace and without allocation: split-K
+// partial sums in a scratch array the library holds on each GPU.
+// ---------------------------------------------------------------------------
+namespace {
+
+// Each GPU the library runs on holds its own copy of this array until the
+// process ends.  In host code the name is only a symbol handle, never an
+// address: the device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) float scratch[LAQ_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+constexpr int kScratchDevices = 64;
+std::atomic<float*> g_scratch_ptr[kScratchDevices];
+std::mutex g_scratch_mutex;
+
+// Device address of `scratch` on the device that runs `stream` (looked up
+// once per device, with that device current).
+laq_status scratch_on_stream_device(const char* fn, hipStream_t stream, float** out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return fail(LAQ_ERR_HIP, fn, hipGetErrorString(e));
+  int dev = cur;
+  if (stream) {
+    hipDevice_t d = 0;
+    e = hipStreamGetDevice(stream, &d);
+    if (e != hipSuccess) return fail(LAQ_ERR_HIP, fn, hipGetErrorString(e));
+    dev = (int)d;
+  }
+  if (dev < 0 || dev >= kScratchDevices) return fail(LAQ_ERR_HIP, fn, "device index beyond the scratch table");
+  float* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return fail(LAQ_ERR_HIP, fn, hipGetErrorString(e));
+      void* addr = nullptr;
+      e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+      const hipError_t e2 = dev != cur ? hipSetDevice(cur) : hipSuccess;
+      if (e != hipSuccess) return fail(LAQ_ERR_HIP, fn, hipGetErrorString(e));
+      if (e2 != hipSuccess) return fail(LAQ_ERR_HIP, fn, hipGetErrorString(e2));
+      if (!addr) return fail(LAQ_ERR_HIP, fn, "no device address for the scratch array");
+      p = static_cast<float*>(addr);
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return LAQ_OK;
+}
+
+}  // namespace
+
+extern "C" laq_status laq_linear_noalloc_w3g128(const void* x, const uint32_t* qweight, const void* scales,
+                                                const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                                                void* stream) {
+  const char* fn = "laq_linear_noalloc_w3g128";
+  const laq::LaunchEvents ev = take_events();  // consumed whether or not the call launches
+  if (!x || !qweight || !scales || !zeros || !y) return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (M < 1 || M > LAQ_MAX_M) return fail(LAQ_ERR_BAD_M, fn, "M must be in 1..16");
+  if (!aligned(x, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "x and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  const size_t need = laq::split_workspace_bytes(laq::mfma_split_plan((int)M, N, (int)(K / 128)), (int)M, N);
+  if (need > (size_t)LAQ_NOALLOC_SCRATCH_BYTES)
+    return fail(LAQ_ERR_BAD_SHAPE, fn,
+                "the split-K partial sums of this shape exceed the scratch array (LAQ_NOALLOC_SCRATCH_BYTES)");
+  float* ws = nullptr;
+  if (need > 0) {
+    st = scratch_on_stream_device(fn, static_cast<hipStream_t>(stream), &ws);
+    if (st != LAQ_OK) return st;
+  }
+  return hip_status(fn, laq::launch_linear<3>(static_cast<const uint16_t*>(x), qweight,
+                                              static_cast<const uint16_t*>(scales), zeros,
+                                              static_cast<uint16_t*>(y), (int)M, N, K,
+                                              static_cast<hipStream_t>(stream), ev, ws, need));
+}

@@ -21,6 +21,7 @@ MAX_M = 16
 GROUP = 128
 
 MAX_GROUP = 8
+NOALLOC_SCRATCH_BYTES = 8 << 20  # LAQ_NOALLOC_SCRATCH_BYTES
 
 EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profile_next_launch",
            "laq_quantize_w3g128", "laq_pack_w3g128", "laq_linear_w3g128", "laq_linear_group_w3g128",
@@ -28,7 +29,7 @@ EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profil
            "laq_linear_workspace_bytes", "laq_linear_ws_w3g128", "laq_linear_ws_w4g128",
            "laq_add_rmsnorm_f16", "laq_qk_norm_rope_f16", "laq_decode_attention_workspace_bytes",
            "laq_decode_attention_f16", "laq_silu_mul_f16", "laq_linear_swiglu_w3g128",
-           "laq_linear_swiglu_w4g128")
+           "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128")
 HEAD_DIM = 128
 
 
@@ -76,7 +77,7 @@ def lib():
             f.argtypes = [ctypes.POINTER(LinearCall), ctypes.c_int32, I64, P]
             f.restype = ctypes.c_int32
         for name in ("laq_linear_w3g128", "laq_linear_w4g128", "laq_linear_swiglu_w3g128",
-                     "laq_linear_swiglu_w4g128"):
+                     "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, P, P, I64, I64, I64, P]
             f.restype = ctypes.c_int32
@@ -192,6 +193,22 @@ def linear(x, qweight, scales, zeros, bits=3, out=None, split_k=True):
         return y
     fn = lib().laq_linear_w3g128 if bits == 3 else lib().laq_linear_w4g128
     _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K, _stream(x.device)))
+    return y
+
+
+def linear_noalloc_w3g128(x, qweight, scales, zeros, out=None):
+    """The W3 linear with split-K partial sums in the library's own scratch
+    array (laq_linear_noalloc_w3g128): no workspace is allocated for it."""
+    import torch
+    assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.is_contiguous()
+    M, K = x.shape
+    N = scales.shape[0]
+    assert qweight.numel() == packed_words(3, N, K) and qweight.is_contiguous()
+    assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+    assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+    y = torch.empty((M, N), dtype=torch.float16, device=x.device) if out is None else out
+    _check(lib().laq_linear_noalloc_w3g128(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K,
+                                           _stream(x.device)))
     return y
 
 

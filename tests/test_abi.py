@@ -177,6 +177,30 @@ def test_linear_ws_validation(L, bits):
     assert b"laq_linear_ws" in L.laq_last_error()
 
 
+def _lin_na(L, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, M=2, N=4, K=128):
+    return L.laq_linear_noalloc_w3g128(ctypes.c_void_p(x), ctypes.c_void_p(q), ctypes.c_void_p(s),
+                                       ctypes.c_void_p(z), ctypes.c_void_p(y), M, N, K, None)
+
+
+def test_linear_noalloc_validation(L):
+    """The no-allocation linear validates like laq_linear_w3g128 and rejects,
+    on the host, shapes whose split-K partial sums exceed its scratch array."""
+    for kw in ("x", "q", "s", "z", "y"):
+        assert _lin_na(L, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _lin_na(L, M=0) == laq.LAQ_ERR_BAD_M
+    assert _lin_na(L, M=17) == laq.LAQ_ERR_BAD_M
+    assert _lin_na(L, K=200) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lin_na(L, x=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert _lin_na(L, y=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    # 410 K ranges x 16 x 16000 fp32 partials = 420 MB > 8 MiB of scratch
+    need = L.laq_linear_workspace_bytes(16, 16000, 1 << 20)
+    assert need > laq.NOALLOC_SCRATCH_BYTES
+    assert _lin_na(L, M=16, N=16000, K=1 << 20) == laq.LAQ_ERR_BAD_SHAPE
+    assert b"scratch" in L.laq_last_error()
+    # the largest split of the Qwen3-32B stack (down projection, M = 16) fits
+    assert 0 < L.laq_linear_workspace_bytes(16, 5120, 25600) <= laq.NOALLOC_SCRATCH_BYTES
+
+
 def test_workspace_bytes(L):
     """The workspace holds S fp32 partial planes of M x N, one per K range of
     at most five quads (512-column blocks), when the row has at least 40 quads
