@@ -4,7 +4,8 @@ Each layer: residual add + RMSNorm, the fused q|k|v linear, per-head q/k
 RMSNorm + rotary embedding + KV-cache append, attention over the cache, the
 o linear, residual add + RMSNorm, the fused gate|up linear, SiLU-and-multiply,
 the down linear (whose output the next layer's first norm adds to the
-residual).  The step ends with the final norm; the LM head is not part of it.
+residual).  The step ends with the final norm and, when one is given, the
+LM head (one more caller-supplied linear, hidden -> vocabulary logits).
 Argument marshalling only: every operation is a call of liblaq.so, except the
 linears, which the caller supplies (the library's quantized linear, or any
 other implementation of y = x W^T to compare against).
@@ -17,7 +18,7 @@ HEAD_DIM = laq.HEAD_DIM
 
 # Qwen3-4B decoder shape (hidden, query heads, key/value heads, MLP width).
 QWEN3_4B = {"layers": 36, "hidden": 2560, "heads": 32, "kv_heads": 8, "mlp": 9728,
-            "eps": 1e-6, "rope_theta": 1e6}
+            "eps": 1e-6, "rope_theta": 1e6, "vocab": 151936}
 
 
 def rope_table(S_max, theta, device, d=HEAD_DIM):
@@ -38,10 +39,12 @@ class DecodeStep:
     itself (laq.linear_swiglu), and the step skips silu_mul.  norms[l] =
     (input_norm, post_attention_norm, q_norm, k_norm) fp16 vectors;
     final_norm fp16 [hidden].  k_caches / v_caches: fp16 [kv_heads][S_max][128]
-    per layer (positions below the decoded one already filled).
+    per layer (positions below the decoded one already filled).  lm_head:
+    optional callable f(x, out) writing the logits out = x W^T (fp16
+    [1][vocab], vocab = shape["vocab"]) from the final norm's output.
     """
 
-    def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device):
+    def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None):
         import torch
         self.s = shape
         self.linears, self.norms, self.final_norm = linears, norms, final_norm
@@ -62,10 +65,14 @@ class DecodeStep:
         self.m = torch.empty((1, I), **f16)
         self.down = torch.empty((1, D), **f16)
         self.out = torch.empty((1, D), **f16)
+        self.lm_head = lm_head
+        self.logits = torch.empty((1, shape["vocab"]), **f16) if lm_head is not None else None
         self.workspace = torch.empty(laq.attention_workspace_bytes(Hq, S_max), dtype=torch.uint8, device=device)
 
     def run(self, pos):
-        """Decode the token at position pos (attends to positions 0..pos)."""
+        """Decode the token at position pos (attends to positions 0..pos).
+        Returns the logits when the step has an LM head, else the final
+        norm's output."""
         s = self.s
         Hq, Hkv, eps = s["heads"], s["kv_heads"], s["eps"]
         self.residual.copy_(self.x0)
@@ -88,4 +95,7 @@ class DecodeStep:
             f_down(self.m, self.down)
             delta = self.down
         laq.add_rmsnorm(self.residual, delta, self.final_norm, eps, out=self.out)
-        return self.out
+        if self.lm_head is None:
+            return self.out
+        self.lm_head(self.out, self.logits)
+        return self.logits

@@ -188,86 +188,145 @@ def test_decoder_layer_4b():
     assert np.allclose(r_mid, r_ref, rtol=1e-6, atol=1e-5)
 
 
-def test_decode_step_graph_replay():
+def _quantized(N, K, cfg, layer, proj, interleave_halves=False):
+    """Oracle-quantized W3 weights of one projection: (codes, scales, zeros)
+    on the host and (qweight, scales, zeros) on the GPU.  interleave_halves:
+    rows reordered gate 0, up 0, gate 1, ... (quantization is per row)."""
+    w = inputs.weights(N, K, cfg=cfg, layer=layer, proj=proj)
+    if interleave_halves:
+        w = np.stack([w[: N // 2], w[N // 2:]], axis=1).reshape(N, K)
+    codes, s, z = oracle.quantize(w, 3)
+    return (codes, s, z), (dev(oracle.pack(codes, 3).view(np.int32)), dev(s.view(np.float16)), dev(z))
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_decode_step_vs_oracle(fused):
     """paper_2605_08755_amd.decode.DecodeStep over two Qwen3-4B-shaped layers
-    with W3 linears: HIP-graph replays equal the eager step bitwise, and the
-    step equals the same calls issued one by one."""
-    say("decode step graph")
+    plus an LM head (4096 vocabulary rows), W3 linears on oracle-quantized
+    codes, at position 200 of a filled cache, against the oracle's
+    composition: every stage of every layer (norms, q|k|v, the rotated q and
+    the cache rows written, attention, o, gate|up or the fused gate|up +
+    SiLU, down, the residual stream, the final norm and the logits) is
+    checked against oracle/decode.py and the oracle's linear applied to the
+    GPU's own fp16 input of that stage, within the linear tolerance (1e-3 x
+    output RMS before the output's fp16 rounding; the fp32 residual stream
+    to 1e-6 relative).  fused: the gate|up linear with SiLU-and-multiply in
+    its output stage.  Then the step (no recording) is captured in a HIP
+    graph: three replays, with eager steps between them, each give logits
+    bitwise equal to the checked eager step."""
+    say("decode step vs oracle, fused =", fused)
     from paper_2605_08755_amd import decode
-    shape = dict(decode.QWEN3_4B, layers=2)
-    D, Hq, Hkv, I, S = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256
-    rng = np.random.default_rng(12)
-    lins, norms, kcs, vcs = [], [], [], []
+    shape = dict(decode.QWEN3_4B, layers=2, vocab=4096)
+    D, Hq, Hkv, I, S, V, pos = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256, 4096, 200
+    rng = np.random.default_rng(13 + fused)
+    host, lins = [], []
     for l in range(2):
-        fs = []
-        for j, (N, K) in enumerate((((Hq + 2 * Hkv) * 128, D), (D, Hq * 128), (2 * I, D), (D, I))):
-            q, s, z = laq.quantize(dev(inputs.weights(N, K, cfg=41, layer=l, proj=j)), 3)
-            fs.append(lambda x, out, q=q, s=s, z=z: laq.linear(x, q, s, z, 3, out=out))
-        lins.append(tuple(fs))
-        norms.append(tuple(dev((1 + 0.1 * rng.standard_normal(n)).astype(np.float16)) for n in (D, D, 128, 128)))
-        kcs.append(dev(f16(rng, (Hkv, S, 128))))
-        vcs.append(dev(f16(rng, (Hkv, S, 128))))
-    fin = dev((1 + 0.1 * rng.standard_normal(D)).astype(np.float16))
-    step = decode.DecodeStep(shape, lins, norms, fin, kcs, vcs, DEV)
-    step.x0.copy_(dev(rng.standard_normal((1, D)).astype(np.float32)))
-    pos = 200
-    eager = step.run(pos).clone()
-    torch.cuda.synchronize()
-    assert torch.isfinite(eager.float()).all()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
-        step.run(pos)
-    for _ in range(3):
-        step.out.zero_()
-        torch.cuda.synchronize()
-        g.replay()
-        torch.cuda.synchronize()
-        assert torch.equal(step.out.view(torch.int16), eager.view(torch.int16))
-        step.run(pos)  # eager work between replays
-        torch.cuda.synchronize()
-        assert torch.equal(step.out.view(torch.int16), eager.view(torch.int16))
-    del g
-
-
-def test_decode_step_fused_swiglu():
-    """DecodeStep with the gate|up linear that applies SiLU-and-multiply in its
-    output stage (weight rows interleaved gate j, up j) against the same step
-    with the plain gate|up linear followed by silu_mul, over two Qwen3-4B-shaped
-    layers.  The fused call skips the fp16 rounding of gate and up, so the two
-    agree to the fp16 precision of the step, not bitwise."""
-    say("decode step fused swiglu")
-    from paper_2605_08755_amd import decode
-    shape = dict(decode.QWEN3_4B, layers=2)
-    D, Hq, Hkv, I, S = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256
-    rng = np.random.default_rng(13)
-    plain, fused, norms, kcs, vcs = [], [], [], [], []
-    for l in range(2):
-        fs, ff = [], []
-        for j, (N, K) in enumerate((((Hq + 2 * Hkv) * 128, D), (D, Hq * 128), (2 * I, D), (D, I))):
-            w = dev(inputs.weights(N, K, cfg=42, layer=l, proj=j))
-            q, s, z = laq.quantize(w, 3)
-            fs.append(lambda x, out, q=q, s=s, z=z: laq.linear(x, q, s, z, 3, out=out))
-            if j == 2:
-                qi, si, zi = laq.quantize(torch.stack([w[:I], w[I:]], dim=1).reshape(N, K).contiguous(), 3)
-                f = lambda x, out, q=qi, s=si, z=zi: laq.linear_swiglu(x, q, s, z, 3, out=out)
+        hl, fl = {}, []
+        for j, (name, N, K) in enumerate((("qkv", (Hq + 2 * Hkv) * 128, D), ("o", D, Hq * 128),
+                                          ("gu", 2 * I, D), ("down", D, I))):
+            hq, (q, s, z) = _quantized(N, K, 43, l, j, interleave_halves=fused and name == "gu")
+            hl[name] = hq
+            if name == "gu" and fused:
+                f = lambda x, out, q=q, s=s, z=z: laq.linear_swiglu(x, q, s, z, 3, out=out)
                 f.swiglu = True
-                ff.append(f)
             else:
-                ff.append(fs[-1])
-        plain.append(tuple(fs))
-        fused.append(tuple(ff))
-        norms.append(tuple(dev((1 + 0.1 * rng.standard_normal(n)).astype(np.float16)) for n in (D, D, 128, 128)))
-        kcs.append(f16(rng, (Hkv, S, 128)))
-        vcs.append(f16(rng, (Hkv, S, 128)))
-    fin = dev((1 + 0.1 * rng.standard_normal(D)).astype(np.float16))
-    x0 = dev(rng.standard_normal((1, D)).astype(np.float32))
-    outs = []
-    for lins in (plain, fused):
-        step = decode.DecodeStep(shape, lins, norms, fin, [dev(a) for a in kcs], [dev(a) for a in vcs], DEV)
-        step.x0.copy_(x0)
-        outs.append(step.run(200).float().cpu().numpy())
+                f = lambda x, out, q=q, s=s, z=z: laq.linear(x, q, s, z, 3, out=out)
+            fl.append(f)
+        host.append(hl)
+        lins.append(fl)
+    h_lm, (q_lm, s_lm, z_lm) = _quantized(V, D, 43, 9, 0)
+    lm = lambda x, out: laq.linear(x, q_lm, s_lm, z_lm, 3, out=out)
+    norms_h = [tuple((1 + 0.1 * rng.standard_normal(n)).astype(np.float16) for n in (D, D, 128, 128))
+               for _ in range(2)]
+    fin_h = (1 + 0.1 * rng.standard_normal(D)).astype(np.float16)
+    kc_h = [f16(rng, (Hkv, S, 128)) for _ in range(2)]
+    vc_h = [f16(rng, (Hkv, S, 128)) for _ in range(2)]
+    x0_h = rng.standard_normal((1, D)).astype(np.float32)
+    norms = [tuple(dev(a) for a in nl) for nl in norms_h]
+    kcs, vcs = [dev(a) for a in kc_h], [dev(a) for a in vc_h]
+
+    rec = []
+
+    def recording(kind, l, f):
+        def g(x, out):
+            f(x, out)
+            e = {"kind": kind, "layer": l, "x": x.clone(), "out": out.clone(), "res": step.residual.clone()}
+            if kind == "o":
+                e["q"] = step.q.clone()
+            rec.append(e)
+        g.swiglu = getattr(f, "swiglu", False)
+        return g
+
+    names = ("qkv", "o", "gu", "down")
+    rec_lins = [tuple(recording(names[j], l, lins[l][j]) for j in range(4)) for l in range(2)]
+    step = decode.DecodeStep(shape, rec_lins, norms, dev(fin_h), kcs, vcs, DEV, lm_head=recording("lm", 2, lm))
+    step.x0.copy_(dev(x0_h))
+    logits = step.run(pos).clone()
+    torch.cuda.synchronize()
+    g = {(e["kind"], e["layer"]): {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in e.items()}
+         for e in rec}
+    assert len(g) == 9
+
+    def check(name, got, ref):
+        r = linear_check(got, ref)
+        assert r["ok"], (name, r)
+
+    def lin(xh, hq):
+        return oracle.linear(xh, *hq)
+
+    r_ref = x0_h.astype(np.float64)
+    for l in range(2):
+        w_in, w_post, qn, kn = norms_h[l]
+        e_qkv, e_o, e_gu, e_dn = (g[(k, l)] for k in names)
+        if l > 0:
+            r_ref = g[("gu", l - 1)]["res"].astype(np.float64) + g[("down", l - 1)]["out"].astype(np.float64)
+        assert np.allclose(e_qkv["res"], r_ref, rtol=1e-6, atol=1e-6), ("residual", l)
+        check(("h", l), e_qkv["x"], OD.rmsnorm(e_qkv["res"], w_in, EPS))
+        check(("qkv", l), e_qkv["out"], lin(e_qkv["x"], host[l]["qkv"]))
+        q_ref, k_ref, v_ref = OD.qk_norm_rope(e_qkv["out"], qn, kn, pos, Hq, Hkv, 128, EPS, THETA)
+        check(("q", l), e_o["q"], q_ref)
+        kc, vc = kcs[l].cpu().numpy(), vcs[l].cpu().numpy()
+        check(("k cache row", l), kc[:, pos], k_ref)
+        assert np.array_equal(vc[:, pos], v_ref.astype(np.float16)), ("v cache row", l)
+        others = np.arange(S) != pos
+        assert np.array_equal(kc[:, others], kc_h[l][:, others]) and np.array_equal(vc[:, others], vc_h[l][:, others])
+        check(("attention", l), e_o["x"].reshape(Hq, 128),
+              OD.decode_attention(e_o["q"], kc[:, :pos + 1], vc[:, :pos + 1]))
+        check(("o", l), e_o["out"], lin(e_o["x"], host[l]["o"]))
+        assert np.allclose(e_gu["res"], e_o["res"].astype(np.float64) + e_o["out"].astype(np.float64),
+                           rtol=1e-6, atol=1e-6), ("residual + o", l)
+        check(("h2", l), e_gu["x"], OD.rmsnorm(e_gu["res"], w_post, EPS))
+        gu_ref = lin(e_gu["x"], host[l]["gu"])
+        if fused:
+            # rows interleaved gate j, up j: the oracle's unrounded sums, then SiLU-and-multiply
+            check(("gate|up + silu", l), e_gu["out"],
+                  OD.silu_mul(np.concatenate([gu_ref[:, 0::2], gu_ref[:, 1::2]], axis=1), I))
+            assert np.array_equal(e_dn["x"], e_gu["out"])
+        else:
+            check(("gate|up", l), e_gu["out"], gu_ref)
+            check(("silu_mul", l), e_dn["x"], OD.silu_mul(e_gu["out"], I))
+        check(("down", l), e_dn["out"], lin(e_dn["x"], host[l]["down"]))
+    r_fin = g[("gu", 1)]["res"].astype(np.float64) + g[("down", 1)]["out"].astype(np.float64)
+    assert np.allclose(step.residual.cpu().numpy(), r_fin, rtol=1e-6, atol=1e-6)
+    check("final norm", g[("lm", 2)]["x"], OD.rmsnorm(r_fin, fin_h, EPS))
+    check("logits", logits.cpu().numpy(), lin(g[("lm", 2)]["x"], h_lm))
+
+    # the same step without recording, captured in a HIP graph
+    gstep = decode.DecodeStep(shape, [tuple(f) for f in lins], norms, dev(fin_h), kcs, vcs, DEV, lm_head=lm)
+    gstep.x0.copy_(dev(x0_h))
+    eager = gstep.run(pos).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(eager.view(torch.int16), logits.view(torch.int16))
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        gstep.run(pos)
+    for _ in range(3):
+        gstep.logits.zero_()
         torch.cuda.synchronize()
-    a, b = outs
-    assert np.isfinite(b).all()
-    rms = float(np.sqrt(np.mean(a ** 2)))
-    assert float(np.abs(a - b).max()) <= 1e-2 * rms, (float(np.abs(a - b).max()), rms)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(gstep.logits.view(torch.int16), logits.view(torch.int16))
+        gstep.run(pos)  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(gstep.logits.view(torch.int16), logits.view(torch.int16))
+    del graph
