@@ -32,20 +32,37 @@ HBM_PEAK_GBS = 8000.0
 GROUP = 128
 
 
+KERNEL_SOURCES = ("paper_2605_08755_amd/csrc/linear.hip", "paper_2605_08755_amd/csrc/laq_internal.h")
+
+
+def kernel_code_digest():
+    """sha256 of the GEMV's sources with comments and blank space removed, so
+    that a comment-only edit keeps the HBM-counter record valid while any
+    change of the code invalidates it."""
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel)) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
+    return h.hexdigest()
+
+
 def measured_traffic():
     """HBM bytes per GEMV launch from the committed rocprofv3 counter runs
-    (profiles/hbm_traffic.json), or None when the kernel source has changed
+    (profiles/hbm_traffic.json), or None when the kernel code has changed
     since those counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         with open(path) as f:
             rec = json.load(f)
-        with open(os.path.join(ROOT, rec["kernel_source"]), "rb") as f:
-            digest = hashlib.sha256(f.read()).hexdigest()
+        digest = kernel_code_digest()
     except (OSError, KeyError, ValueError):
         return None
-    if digest != rec.get("kernel_source_sha256"):
+    if digest != rec.get("kernel_code_digest"):
         return None
     return rec
 
@@ -245,10 +262,13 @@ def time_fp16_graph(stack, M, steps, warmup):
 def decode_step_extra(stack, dev, steps, context=1024):
     """One batch-1 decode step of the Qwen3-4B-shaped decoder (36 layers:
     norms, rotary embedding, attention over a synthetic KV cache of `context`
-    positions, SiLU-and-multiply, and the stack's linears), the token at
-    position context - 1, captured in a HIP graph: with the W3 linears, and
-    with the fp16 weights through torch's dense GEMM for the unquantized
-    reference.  The LM head is not part of the step."""
+    positions, SiLU-and-multiply, the stack's linears, the final norm and the
+    LM head over Qwen3-4B's 151936-token vocabulary), the token at position
+    context - 1, captured in a HIP graph.  Variants: W3 linears and a W3 LM
+    head; W3 with the gate|up + SiLU linear and a W3 or an fp16 LM head; fp16
+    weights everywhere through torch's dense GEMM (the unquantized
+    reference).  The paper does not say whether its decoding benchmark
+    quantizes the LM head, hence both heads."""
     import torch
     from paper_2605_08755_amd import decode, inputs, laq
     shape = dict(decode.QWEN3_4B)
@@ -259,10 +279,12 @@ def decode_step_extra(stack, dev, steps, context=1024):
     def vec(n):
         return (1.0 + 0.1 * torch.randn((n,), generator=g, device=dev)).to(torch.float16)
 
-    D, Hkv = shape["hidden"], shape["kv_heads"]
+    D, Hkv, V = shape["hidden"], shape["kv_heads"], shape["vocab"]
     norms = [(vec(D), vec(D), vec(128), vec(128)) for _ in range(shape["layers"])]
     caches = [torch.randn((2, Hkv, context, 128), generator=g, device=dev).to(torch.float16)
               for _ in range(shape["layers"])]
+    w_head = inputs.weights_torch(V, D, seed=999999, device=dev)
+    q_head = laq.quantize(w_head, 3)
 
     def w3_lin(i):
         q, sc, z = stack.q[3][i]
@@ -285,17 +307,22 @@ def decode_step_extra(stack, dev, steps, context=1024):
         f.swiglu = True
         return f
 
-    out = {"context": context, "layers": shape["layers"]}
-    for name, mk in (("w3", w3_lin), ("w3_fused_swiglu", w3_swiglu_lin), ("fp16", fp16_lin)):
+    head_w3 = lambda x, out: laq.linear(x, *q_head, 3, out=out)
+    head_fp16 = lambda x, out: torch.mm(x, w_head.t(), out=out)
+    out = {"context": context, "layers": shape["layers"], "vocab": V}
+    variants = (("w3", w3_lin, head_w3), ("w3_fused_swiglu", w3_swiglu_lin, head_w3),
+                ("w3_fused_swiglu_fp16_head", w3_swiglu_lin, head_fp16), ("fp16", fp16_lin, head_fp16))
+    for name, mk, head in variants:
         lins = [tuple(mk(4 * l + j) for j in range(4)) for l in range(shape["layers"])]
-        step = decode.DecodeStep(shape, lins, norms, vec(D), [c[0] for c in caches], [c[1] for c in caches], dev)
+        step = decode.DecodeStep(shape, lins, norms, vec(D), [c[0] for c in caches], [c[1] for c in caches], dev,
+                                 lm_head=head)
         step.x0.copy_(torch.randn((1, D), generator=g, device=dev))
         ms, _ = time_graph(stack, 1, 3, steps, 5, step_fn=lambda: step.run(context - 1))
         out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}
         del step
     swiglu_w.clear()
-    out["w3_speedup_vs_fp16"] = round(out["fp16"]["us"] / out["w3"]["us"], 3)
-    out["w3_fused_swiglu_speedup_vs_fp16"] = round(out["fp16"]["us"] / out["w3_fused_swiglu"]["us"], 3)
+    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fp16_head"):
+        out[name + "_speedup_vs_fp16"] = round(out["fp16"]["us"] / out[name]["us"], 3)
     return out
 
 
@@ -328,6 +355,154 @@ def stack32b_extra(dev, steps):
     return out
 
 
+def per_call_graph(stack, M, bits, reps=20):
+    """Per call shape: a HIP graph of that shape's calls of every layer, back
+    to back (distinct weights, as in the step); µs per call and algorithmic
+    GB/s.  The one per-projection figure that includes no event or launch
+    overhead beyond the dependent-launch gap of the step itself."""
+    import torch
+    from paper_2605_08755_amd import laq
+    out = {}
+    for gname in [g[0] for g in stack.groups]:
+        idx = [i for i, sh in enumerate(stack.shapes) if sh[1] == gname]
+        N, K = stack.shapes[idx[0]][2], stack.shapes[idx[0]][3]
+
+        def fn():
+            for i in idx:
+                layer = stack.shapes[i][0]
+                q, sc, z = stack.q[bits][i]
+                laq.linear(stack.x[(layer, stack.slot_of[i])][:M], q, sc, z, bits, out=stack.y[i][:M])
+        ms = time_calls_graph(fn, reps=reps)
+        us = ms * 1e3 / len(idx)
+        out[gname] = {"N": N, "K": K, "us": round(us, 3),
+                      "GBps": round(N * K * bytes_per_weight(bits) / (us * 1e-6) / 1e9, 1)}
+    return out
+
+
+def single_extra(dev, reps=20):
+    """The single 1024 x 1024 W3G128 linear at M = 1: µs per call with the
+    same weights every call (0.42 MB, cache-resident: the latency-bound
+    figure), and over 2400 rotated copies (1.0 GB streamed from HBM per pass)
+    for an HBM rate; quantize µs per call."""
+    import torch
+    from paper_2605_08755_amd import inputs, laq
+    N = K = 1024
+    w = inputs.weights_torch(N, K, seed=77, device=dev)
+    q, sc, z = laq.quantize(w, 3)
+    x = inputs.activations_torch(1, K, seed=77, device=dev)
+    y = torch.empty((1, N), dtype=torch.float16, device=dev)
+
+    def same():
+        for _ in range(1000):
+            laq.linear(x, q, sc, z, 3, out=y)
+    us_same = time_calls_graph(same, reps=reps) * 1e3 / 1000
+    copies = 2400
+    ws = [laq.quantize(inputs.weights_torch(N, K, seed=1000 + i, device=dev), 3) for i in range(copies)]
+
+    def rotated():
+        for (qq, ss, zz) in ws:
+            laq.linear(x, qq, ss, zz, 3, out=y)
+    us_rot = time_calls_graph(rotated, reps=3) * 1e3 / copies
+    qout = (torch.empty_like(q), torch.empty_like(sc), torch.empty_like(z))
+
+    def quant():
+        for _ in range(200):
+            laq.quantize(w, 3, out=qout)
+    us_q = time_calls_graph(quant, reps=reps) * 1e3 / 200
+    del ws
+    torch.cuda.empty_cache()
+    wb = N * K * bytes_per_weight(3)
+    return {"shape": "N=1024, K=1024, M=1, W3G128", "weight_bytes": int(wb),
+            "linear_us_same_weights": round(us_same, 3),
+            "linear_us_rotated_1GB": round(us_rot, 3),
+            "linear_GBps_rotated": round(wb / (us_rot * 1e-6) / 1e9, 1),
+            "quantize_us": round(us_q, 3)}
+
+
+def trace_run(args, dev):
+    """Workload for rocprofv3 --kernel-trace: the headline step (W3, M = 1,
+    144 dependent GEMV launches), one eager warm-up step, then --warmup +
+    --steps replays of its HIP graph, nothing else.  --summarize-trace reads
+    the resulting kernel_trace.csv."""
+    import torch
+    stack = Stack(args.workload, dev, bits_list=(3,), fused=not args.unfused)
+    ms, _ = time_graph(stack, 1, 3, args.steps, args.warmup)
+    print("trace run: %d launches per step, %d graph replays (%d warm-up), %.2f us/step by HIP events"
+          % (len(stack.shapes), args.steps + args.warmup, args.warmup, ms * 1e3), flush=True)
+
+
+def summarize_trace(path, launches, steps):
+    """Markdown summary of a rocprofv3 kernel_trace.csv from --trace-run:
+    per-dispatch durations of the GEMV over the last `steps` graph replays
+    (by call shape: grid size), and per replay the span from the first
+    dispatch's start to the last one's end."""
+    import csv
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if "linear" in r["Kernel_Name"]:
+                rows.append(r)
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    rows = rows[-launches * steps:]
+    assert len(rows) == launches * steps, (len(rows), launches * steps)
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    spans, sums, gaps = [], [], []
+    for i in range(steps):
+        st = rows[i * launches:(i + 1) * launches]
+        spans.append((int(st[-1]["End_Timestamp"]) - int(st[0]["Start_Timestamp"])) / 1e3)
+        sums.append(sum(durs[i * launches:(i + 1) * launches]))
+    by = {}
+    for r, d in zip(rows, durs):
+        key = (r["Kernel_Name"].split("(")[0][-60:], r.get("Grid_Size_X", r.get("Grid_Size", "")))
+        by.setdefault(key, []).append(d)
+    med = lambda v: sorted(v)[len(v) // 2]
+    lines = ["| kernel (name tail) | grid | dispatches | avg µs | p50 µs | min µs |", "|---|---|---|---|---|---|"]
+    for (k, g), v in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        lines.append("| %s | %s | %d | %.3f | %.3f | %.3f |" % (k, g, len(v), sum(v) / len(v), med(v), min(v)))
+    lines.append("")
+    lines.append("Per graph replay (%d replays, %d GEMV dispatches each): first start to last end %.1f µs "
+                 "(p50 %.1f), i.e. %.3f µs per launch; sum of dispatch durations %.1f µs (p50 %.1f), "
+                 "%.3f µs per dispatch."
+                 % (steps, launches, sum(spans) / steps, med(spans), sum(spans) / steps / launches,
+                    sum(sums) / steps, med(sums), sum(sums) / steps / launches))
+    return "\n".join(lines)
+
+
+def pmc_summary(fetch_csv, write_csv, launches, steps):
+    """Per-launch HBM bytes of the GEMV from two rocprofv3 --pmc runs of
+    --profile-run (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
+    scaled by what the counter reads for the 256 MiB device copy that
+    --profile-run performs first."""
+    import csv
+
+    def load(path, counter):
+        copy, lin = [], []
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r.get("Counter_Name", counter) != counter:
+                    continue
+                v = float(r["Counter_Value"])
+                name = r["Kernel_Name"]
+                if "linear" in name:
+                    lin.append(v)
+                elif "copy" in name.lower() or "elementwise" in name.lower():
+                    copy.append(v)
+        return copy, lin
+    cf, lf = load(fetch_csv, "FETCH_SIZE")
+    cw, lw = load(write_csv, "WRITE_SIZE")
+    nbytes_kib = (256 << 20) / 1024
+    fscale = nbytes_kib / max(cf)
+    wscale = nbytes_kib / max(cw)
+    lf, lw = lf[-launches * steps:], lw[-launches * steps:]
+    fetch = sum(lf) / len(lf) * fscale * 1024
+    write = sum(lw) / len(lw) * wscale * 1024
+    return {"fetch_scale": round(fscale, 4), "write_scale": round(wscale, 4),
+            "calibration": "256 MiB device copy: FETCH_SIZE %.0f KiB, WRITE_SIZE %.0f KiB (read and written: "
+                           "%.0f KiB each)" % (max(cf), max(cw), nbytes_kib),
+            "fetch_bytes_per_launch": int(round(fetch)), "write_bytes_per_launch": int(round(write)),
+            "hbm_bytes_per_launch": int(round(fetch + write)), "dispatches": len(lf)}
+
+
 def kernel_durations(stack, M, bits, reps):
     """Per-launch kernel durations (ms) from events recorded at kernel start/end."""
     import torch
@@ -346,14 +521,26 @@ def kernel_durations(stack, M, bits, reps):
     return [t / reps for t in tot]
 
 
-def cpu_baseline(budget_s=12.0):
-    """The CPU oracle (as it stands) on a bounded sample: layer 0 of the
-    Qwen3-4B stack (7 projections, M = 1), repeated for ~budget_s seconds."""
-    import numpy as np
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_layer_rate(budget_s, projs=None):
+    """(GB/s, seconds per layer, repetitions, weights) of the oracle's fp64
+    linear over layer 0 of the Qwen3-4B stack (or the projections named)."""
     import oracle
     from paper_2605_08755_amd import inputs
     cases = []
     for pi, (name, N, K) in enumerate(inputs.QWEN3_4B):
+        if projs is not None and name not in projs:
+            continue
         w = inputs.weights(N, K, cfg=3, layer=0, proj=pi)
         codes, s, z = oracle.quantize(w, 3)
         x = inputs.activations(1, K, cfg=3, layer=0, slot=inputs.X_SLOT[name])
@@ -369,13 +556,38 @@ def cpu_baseline(budget_s=12.0):
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = (time.perf_counter() - t0) / reps
-    gbs = weights * bytes_per_weight(3) / dt / 1e9
+    return weights * bytes_per_weight(3) / dt / 1e9, dt, reps, weights
+
+
+def cpu_baseline(budget_s=12.0):
+    """The CPU oracle (as it stands) on a bounded sample: layer 0 of the
+    Qwen3-4B stack (7 projections, M = 1), repeated for ~budget_s seconds on
+    all host threads; and the k projection alone on one thread (a child
+    process with OMP_NUM_THREADS=1)."""
+    import subprocess
+    import oracle
+    gbs, dt, reps, weights = _oracle_layer_rate(budget_s)
+    one = None
+    try:
+        code = ("import sys, json; sys.path.insert(0, %r); import bench, oracle; "
+                "r = bench._oracle_layer_rate(4.0, projs=('k',)); "
+                "print(json.dumps([r[0], r[1], r[2], r[3], oracle.num_threads()]))" % ROOT)
+        env = dict(os.environ, OMP_NUM_THREADS="1")
+        r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
+        v = json.loads(r.stdout.strip().splitlines()[-1])
+        one = {"value": round(v[0], 4), "unit": "GB/s", "cores": v[4],
+               "sample": "the k projection of layer 0 (1024 x 2560, %d weights), %d repetitions, %.1f ms each"
+                         % (v[3], v[2], v[1] * 1e3)}
+    except Exception as e:  # the one-thread figure is informative only
+        one = {"error": str(e)[:200]}
     return {"value": round(gbs, 3), "unit": "GB/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": "layer 0 of the 36-layer Qwen3-4B-shaped stack: 7 W3G128 projections "
                       "(%d weights) at M=1, oracle fp64 linear on its own codes, %d repetitions "
                       "in %.1f s; %.1f ms per layer, i.e. %.0f ms per 36-layer step"
                       % (weights, reps, dt * reps, dt * 1e3, dt * 36e3),
-            "us_per_step_equiv": round(dt * 36e6, 1)}
+            "us_per_step_equiv": round(dt * 36e6, 1),
+            "one_thread": one}
 
 
 def profile_run(args, dev):
@@ -414,7 +626,23 @@ def main():
     ap.add_argument("--profile-m", type=int, default=1, help="activation rows of the --profile-run steps (1..16)")
     ap.add_argument("--unfused", action="store_true",
                     help="one call per projection (7 per layer) instead of one per shared-input stage (4)")
+    ap.add_argument("--trace-run", action="store_true",
+                    help="for rocprofv3 --kernel-trace: the headline step's graph, --warmup + --steps replays only")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print a markdown summary of a --trace-run kernel trace (last --steps replays) and exit")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the per-launch HBM bytes of --profile-run counter collections and exit")
+    ap.add_argument("--launches", type=int, default=144, help="GEMV launches per step (for the summaries)")
     args = ap.parse_args()
+
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.launches, args.steps))
+        return
+    if args.pmc_summary:
+        rec = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.launches, args.steps)
+        rec["kernel_code_digest"] = kernel_code_digest()
+        print(json.dumps(rec, indent=1))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this library's path runs on a single MI355X "
@@ -429,6 +657,9 @@ def main():
 
     if args.profile_run:
         profile_run(args, dev)
+        return
+    if args.trace_run:
+        trace_run(args, dev)
         return
 
     bits_list = (3,) if args.no_sweep else (3, 4)
@@ -470,7 +701,8 @@ def main():
         ustack = Stack(args.workload, dev, bits_list=(3,), fused=False)
         ums, _ = time_graph(ustack, 1, 3, max(20, args.steps // 4), 5)
         unfused = {"us_per_step": round(ums * 1e3, 2), "launches_per_step": len(ustack.shapes),
-                   "GBps": round(wbytes / (ums * 1e-3) / 1e9, 1)}
+                   "GBps": round(wbytes / (ums * 1e-3) / 1e9, 1),
+                   "per_projection_graph": per_call_graph(ustack, 1, 3)}
         log("unfused (one call per projection):", unfused)
         gms, _ = time_graph(ustack, 1, 3, max(20, args.steps // 4), 5,
                             step_fn=lambda: grouped_step(ustack, 1, 3))
@@ -480,8 +712,10 @@ def main():
         del ustack
         torch.cuda.empty_cache()
 
+    per_call = per_call_graph(stack, 1, 3)
+    log("per call shape (graph of each shape's calls):", per_call)
     extra = {"us_per_step_graph": round(ms * 1e3, 2), "unfused": unfused, "pct_of_hbm_peak": round(value / HBM_PEAK_GBS * 100, 2),
-             "launches_per_step": n_launch,
+             "launches_per_step": n_launch, "per_call_graph": per_call,
              "eager_kernel_events": {"sum_us_per_step": round(ksum_ms * 1e3, 2),
                                      "avg_us": round(ksum_ms * 1e3 / n_launch, 3)},
              "per_projection": per_proj,
@@ -496,6 +730,8 @@ def main():
                                                 "GBps": round(stack.weight_bytes(bits) / (ms_b * 1e-3) / 1e9, 1)}
         extra["sweep"] = sweep
         log("sweep", sweep)
+        extra["single_1024"] = single_extra(dev)
+        log("single 1024 x 1024:", extra["single_1024"])
         # quantize throughput over the whole stack (fp16 read + packed write):
         # all calls captured in one HIP graph (as the linear stack), and the
         # same calls launched eagerly from Python for comparison
