@@ -268,7 +268,9 @@ def decode_step_extra(stack, dev, steps, context=1024):
     head; W3 with the gate|up + SiLU linear and a W3 or an fp16 LM head; fp16
     weights everywhere through torch's dense GEMM (the unquantized
     reference).  The paper does not say whether its decoding benchmark
-    quantizes the LM head, hence both heads."""
+    quantizes the LM head, hence both heads.  Attention is the fused
+    q/k-norm + rotary + attention call except in the _separate_attention
+    variant (qk-norm-rope, attention partials, combine: three kernels)."""
     import torch
     from paper_2605_08755_amd import decode, inputs, laq
     shape = dict(decode.QWEN3_4B)
@@ -310,12 +312,13 @@ def decode_step_extra(stack, dev, steps, context=1024):
     head_w3 = lambda x, out: laq.linear(x, *q_head, 3, out=out)
     head_fp16 = lambda x, out: torch.mm(x, w_head.t(), out=out)
     out = {"context": context, "layers": shape["layers"], "vocab": V}
-    variants = (("w3", w3_lin, head_w3), ("w3_fused_swiglu", w3_swiglu_lin, head_w3),
-                ("w3_fused_swiglu_fp16_head", w3_swiglu_lin, head_fp16), ("fp16", fp16_lin, head_fp16))
-    for name, mk, head in variants:
+    variants = (("w3", w3_lin, head_w3, True), ("w3_fused_swiglu", w3_swiglu_lin, head_w3, True),
+                ("w3_fused_swiglu_separate_attention", w3_swiglu_lin, head_w3, False),
+                ("w3_fused_swiglu_fp16_head", w3_swiglu_lin, head_fp16, True), ("fp16", fp16_lin, head_fp16, True))
+    for name, mk, head, fused_attention in variants:
         lins = [tuple(mk(4 * l + j) for j in range(4)) for l in range(shape["layers"])]
         step = decode.DecodeStep(shape, lins, norms, vec(D), [c[0] for c in caches], [c[1] for c in caches], dev,
-                                 lm_head=head)
+                                 lm_head=head, fused_attention=fused_attention)
         step.x0.copy_(torch.randn((1, D), generator=g, device=dev))
         ms, _ = time_graph(stack, 1, 3, steps, 5, step_fn=lambda: step.run(context - 1))
         out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}

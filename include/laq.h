@@ -369,6 +369,35 @@ laq_status laq_decode_attention_f16(const void *q, const void *k_cache, const vo
                                     int64_t Hkv, int64_t head_dim, int64_t L, int64_t S_max, void *out,
                                     void *workspace, int64_t workspace_bytes, void *stream);
 
+/* laq_decode_attention_qkv_workspace_bytes -- workspace (bytes) with which
+ * laq_decode_attention_qkv_f16 runs for Hq query heads, Hkv key/value heads
+ * and any pos with pos + 1 <= L (so one workspace sized for L = S_max serves a
+ * whole generation); 0 for invalid sizes. */
+int64_t laq_decode_attention_qkv_workspace_bytes(int64_t Hq, int64_t Hkv, int64_t L);
+
+/* laq_decode_attention_qkv_f16 -- laq_qk_norm_rope_f16 followed by
+ * laq_decode_attention_f16 over L = pos + 1 positions, in two kernels
+ * instead of three: from one token's q|k|v projection output qkv (layout as
+ * for laq_qk_norm_rope_f16), each q and k head is RMS-normalized with its
+ * weights and rotated by row pos of cos_sin; k and v are written to row pos of
+ * the caches; then
+ *   out[h] = sum_{t <= pos} softmax_t(q[h] . k[t] / sqrt(128)) v[t]
+ * (fp16 [Hq][128]) with q rounded to fp16 as laq_qk_norm_rope_f16 stores it.
+ * The positions are split into tiles of 16, 32 or 64 (so that short contexts
+ * still occupy the GPU), whose partial results go to the workspace and are
+ * combined in position order.  Results: within the tolerance of the
+ * two-call sequence (the tiles differ), deterministic.
+ *   workspace  [scratch] device memory, 16-byte aligned, any contents, at
+ *              least laq_decode_attention_qkv_workspace_bytes(Hq, Hkv, pos + 1)
+ *              bytes; calls in flight need separate workspaces.
+ * Errors: NULL_POINTER; BAD_SHAPE (head layout as for laq_qk_norm_rope_f16,
+ * pos outside 0..S_max-1, S_max > 2^21, bad eps, workspace too small);
+ * MISALIGNED. */
+laq_status laq_decode_attention_qkv_f16(const void *qkv, const void *q_norm_weight, const void *k_norm_weight,
+                                        const float *cos_sin, int64_t pos, int64_t Hq, int64_t Hkv,
+                                        int64_t head_dim, float eps, void *k_cache, void *v_cache, int64_t S_max,
+                                        void *out, void *workspace, int64_t workspace_bytes, void *stream);
+
 /* laq_silu_mul_f16 -- y[m][i] = fp16(silu(g) * u), g = gate_up[m][i],
  * u = gate_up[m][I + i], silu(g) = g / (1 + exp(-g)): the fused gate|up
  * projection's output fp16 [M][2I] to the down projection's input

@@ -1,6 +1,7 @@
 // C ABI of the library (include/laq.h): argument validation on the host,
 // then an asynchronous launch on the caller's stream.  Nothing is enqueued
 // when validation fails.
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <cstdio>
@@ -306,6 +307,43 @@ laq_status laq_decode_attention_f16(const void* q, const void* k_cache, const vo
                             static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k_cache),
                             static_cast<const uint16_t*>(v_cache), Hq, Hkv, L, S_max, static_cast<uint16_t*>(out),
                             static_cast<float*>(workspace), static_cast<hipStream_t>(stream), ev));
+}
+
+int64_t laq_decode_attention_qkv_workspace_bytes(int64_t Hq, int64_t Hkv, int64_t L) {
+  if (Hq < 1 || Hkv < 1 || L < 1 || Hq > 4096 || Hkv > Hq || L > (1LL << 21)) return 0;
+  // The tile length grows with the context, so the tile count is largest at
+  // the end of a tile-length regime: the maximum over every L' <= L.
+  int64_t tiles = 0;
+  for (int64_t lp : {L, std::min(L, 32767 / Hkv), std::min(L, 4095 / Hkv)})
+    if (lp >= 1) tiles = std::max(tiles, laq::decode_attention_qkv_tiles(Hkv, lp));
+  return Hq * tiles * (kHeadDimAbi + 2) * (int64_t)sizeof(float);
+}
+
+laq_status laq_decode_attention_qkv_f16(const void* qkv, const void* q_norm_weight, const void* k_norm_weight,
+                                        const float* cos_sin, int64_t pos, int64_t Hq, int64_t Hkv,
+                                        int64_t head_dim, float eps, void* k_cache, void* v_cache, int64_t S_max,
+                                        void* out, void* workspace, int64_t workspace_bytes, void* stream) {
+  const char* fn = "laq_decode_attention_qkv_f16";
+  const laq::LaunchEvents ev = take_events();
+  if (!qkv || !q_norm_weight || !k_norm_weight || !cos_sin || !k_cache || !v_cache || !out || !workspace)
+    return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_heads(fn, Hq, Hkv, head_dim);
+  if (st != LAQ_OK) return st;
+  if (S_max < 1 || S_max > (1LL << 21) || pos < 0 || pos >= S_max)
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need 1 <= S_max <= 2^21 and 0 <= pos < S_max");
+  if (!(eps >= 0.0f) || !(eps < INFINITY)) return fail(LAQ_ERR_BAD_SHAPE, fn, "eps must be finite and >= 0");
+  if (workspace_bytes < laq_decode_attention_qkv_workspace_bytes(Hq, Hkv, pos + 1))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "workspace_bytes below laq_decode_attention_qkv_workspace_bytes(Hq, Hkv, pos + 1)");
+  if (!aligned(qkv, 2) || !aligned(q_norm_weight, 2) || !aligned(k_norm_weight, 2) || !aligned(cos_sin, 4) ||
+      !aligned(out, 2) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(workspace, 16))
+    return fail(LAQ_ERR_MISALIGNED, fn,
+                "caches and workspace must be 16-byte, cos_sin 4-byte, fp16 arrays 2-byte aligned");
+  return hip_status(fn, laq::launch_decode_attention_qkv(
+                            static_cast<const uint16_t*>(qkv), static_cast<const uint16_t*>(q_norm_weight),
+                            static_cast<const uint16_t*>(k_norm_weight), cos_sin, pos, Hq, Hkv, eps,
+                            static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache), S_max,
+                            static_cast<uint16_t*>(out), static_cast<float*>(workspace),
+                            static_cast<hipStream_t>(stream), ev));
 }
 
 }  // extern "C"

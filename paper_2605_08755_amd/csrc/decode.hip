@@ -95,6 +95,20 @@ __global__ __launch_bounds__(kNormThreads) void add_rmsnorm_kernel(float* __rest
   for (int i = t; i < D; i += kNormThreads) yr[i] = f2h(r[i] * inv * h2f(w[i]));
 }
 
+// RMSNorm of one 128-value head held by a wave (lane i: dimensions i and
+// i + 64, a and b) with weights wn, then the rotary embedding of the pair
+// (a, b) by the angle whose cosine and sine are cs[i] and cs[64 + i].
+__device__ __forceinline__ void norm_rope_pair(float& a, float& b, const uint16_t* __restrict__ wn,
+                                               const float* __restrict__ cs, float eps, int i) {
+  const float ss = wave_sum(fmaf(a, a, b * b));
+  const float inv = 1.0f / sqrtf(ss / (float)kHeadDim + eps);
+  const float na = a * inv * h2f(wn[i]);
+  const float nb = b * inv * h2f(wn[i + 64]);
+  const float c = cs[i], s = cs[64 + i];
+  a = na * c - nb * s;
+  b = nb * c + na * s;
+}
+
 // One head per block (64 lanes; lane i holds dimensions i and i + 64, the
 // pair the rotary embedding turns): q heads are normalized, rotated and
 // written to q_out, k heads normalized, rotated and written to the key cache
@@ -117,16 +131,11 @@ __global__ __launch_bounds__(64) void qk_norm_rope_kernel(const uint16_t* __rest
     return;
   }
   const bool isq = h < Hq;
-  const uint16_t* wn = isq ? qw : kw;
   float a = h2f(src[i]), b = h2f(src[i + 64]);
-  const float ss = wave_sum(fmaf(a, a, b * b));
-  const float inv = 1.0f / sqrtf(ss / (float)kHeadDim + eps);
-  a = a * inv * h2f(wn[i]);
-  b = b * inv * h2f(wn[i + 64]);
-  const float c = cs[i], s = cs[64 + i];
+  norm_rope_pair(a, b, isq ? qw : kw, cs, eps, i);
   uint16_t* dst = isq ? q_out + (int64_t)h * kHeadDim : kc + ((int64_t)(h - Hq) * S_max + pos) * kHeadDim;
-  dst[i] = f2h(a * c - b * s);
-  dst[i + 64] = f2h(b * c + a * s);
+  dst[i] = f2h(a);
+  dst[i + 64] = f2h(b);
 }
 
 // Partial attention of one key/value head over 64 positions: a block of R
@@ -250,6 +259,205 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
 }
 
 
+// The attention of one decode token straight from the q|k|v projection
+// output: per-head RMSNorm and rotary embedding of q and k, the key/value
+// cache append at pos, and the partial attention over tiles of P positions
+// (L = pos + 1), in one kernel.  Block (g, tile) of R waves, wave w for query
+// head g*R + w:
+//  - issues the tile's cache rows before pos (16-byte loads, all in flight
+//    before the first use; rows at pos and beyond are not loaded),
+//  - normalizes and rotates its query head (rounded to fp16, as the separate
+//    qk-norm-rope call stores it, then scaled by 1/sqrt(128)),
+//  - the block whose tile holds pos also forms that token's key (normalized,
+//    rotated, rounded to fp16) and value, writes them to the caches and into
+//    its tile in LDS,
+//  - scores the tile's positions (64/P lanes per position, each a slice of
+//    the 128 dimensions, added by a fixed butterfly), forms the softmax
+//    statistics and the weighted value sums as attn_partial_kernel does.
+// Partials go to ws[((h * T) + tile) * 130 + {0: m, 1: l, 2..129: o}].
+template <int R, int P>
+__global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
+    const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ qw, const uint16_t* __restrict__ kw,
+    const float* __restrict__ cs, float eps, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int64_t S_max,
+    int pos, int Hq, int Hkv, int T, float* __restrict__ ws) {
+  static_assert(P == 16 || P == 32 || P == 64, "tile of 16, 32 or 64 positions");
+  constexpr int DS = 64 / P;                   // lanes per position (dimension slices)
+  constexpr int kUnits = P * kHeadDim / 8;     // 16-byte units of keys (and of values) per tile
+  constexpr int kThreads = 64 * R;
+  constexpr int kPer = (kUnits + kThreads - 1) / kThreads;
+  __shared__ float qs[R][kHeadDim];
+  __shared__ u32x4 kt[P * kKeyStrideU4];
+  __shared__ u32x4 vt[P * kHeadDim / 8];
+  const int g = blockIdx.x;
+  const int tile = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int L = pos + 1;
+  const int p0 = tile * P;
+  const int nload = max(0, min(P, pos - p0));  // cache rows read from memory
+  const int64_t row0 = (int64_t)g * S_max + p0;
+  const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kc + row0 * kHeadDim),
+                                                                     (short)0, nload * kHeadDim * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(vc + row0 * kHeadDim),
+                                                                     (short)0, nload * kHeadDim * 2, 0x00020000);
+  u32x4 ka[kPer], va[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const uint32_t u = (uint32_t)(i * kThreads + tid);
+    ka[i] = __builtin_amdgcn_raw_buffer_load_b128(kr, u * 16, 0, 0);
+    va[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, u * 16, 0, 0);
+  }
+  // this wave's query head (and, in the block holding pos, wave 0: the new key and value)
+  const uint16_t* qsrc = qkv + (int64_t)(g * R + w) * kHeadDim;
+  float a = h2f(qsrc[lane]), b = h2f(qsrc[lane + 64]);
+  const bool own = pos >= p0 && pos < p0 + P;  // uniform over the block
+  float ka0 = 0.0f, kb0 = 0.0f;
+  uint16_t v0 = 0, v1 = 0;
+  if (own && w == 0) {
+    const uint16_t* ksrc = qkv + (int64_t)(Hq + g) * kHeadDim;
+    const uint16_t* vsrc = qkv + (int64_t)(Hq + Hkv + g) * kHeadDim;
+    ka0 = h2f(ksrc[lane]);
+    kb0 = h2f(ksrc[lane + 64]);
+    v0 = vsrc[lane];
+    v1 = vsrc[lane + 64];
+  }
+  norm_rope_pair(a, b, qw, cs, eps, lane);
+  const float scale = 0.08838834764831845f;  // 1 / sqrt(128)
+  qs[w][lane] = h2f(f2h(a)) * scale;
+  qs[w][lane + 64] = h2f(f2h(b)) * scale;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int u = i * kThreads + tid;
+    if (u < kUnits && (u >> 4) < nload) {
+      kt[(u >> 4) * kKeyStrideU4 + (u & 15)] = ka[i];
+      vt[u] = va[i];
+    }
+  }
+  if (own && w == 0) {
+    norm_rope_pair(ka0, kb0, kw, cs, eps, lane);
+    const uint16_t k0 = f2h(ka0), k1 = f2h(kb0);
+    const int64_t crow = ((int64_t)g * S_max + pos) * kHeadDim;
+    kc[crow + lane] = k0;
+    kc[crow + lane + 64] = k1;
+    vc[crow + lane] = v0;
+    vc[crow + lane + 64] = v1;
+    uint16_t* kl = reinterpret_cast<uint16_t*>(kt + (pos - p0) * kKeyStrideU4);
+    uint16_t* vl = reinterpret_cast<uint16_t*>(vt + (pos - p0) * (kHeadDim / 8));
+    kl[lane] = k0;
+    kl[lane + 64] = k1;
+    vl[lane] = v0;
+    vl[lane + 64] = v1;
+  }
+  __syncthreads();
+
+  // scores: lane = (slice c, position t) with t = lane % P, c = lane / P
+  const int t = lane % P;
+  const int c = lane / P;
+  const int p = p0 + t;
+  const bool valid = p < L;
+  float sc = 0.0f;
+#pragma unroll
+  for (int cc = 0; cc < (kHeadDim / 8) / DS; ++cc) {
+    const int unit = c * ((kHeadDim / 8) / DS) + cc;
+    const u32x4 kv = kt[t * kKeyStrideU4 + unit];
+    const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      sc = fmaf(h2f((uint16_t)(wv[e >> 1] >> (16 * (e & 1)))), qs[w][unit * 8 + e], sc);
+  }
+#pragma unroll
+  for (int o = P; o < 64; o <<= 1) sc += __shfl_xor(sc, o, 64);
+  const float sv = valid && c == 0 ? sc : -INFINITY;
+  const float m = wave_max(sv);
+  const float pr = (valid && c == 0) ? expf(sv - m) : 0.0f;
+  const float l = wave_sum(pr);
+  float o0 = 0.0f, o1 = 0.0f;
+  const uint16_t* vh = reinterpret_cast<const uint16_t*>(vt);
+  const int npos = min(P, L - p0);
+  for (int tt = 0; tt < npos; ++tt) {
+    const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pr), tt));
+    o0 = fmaf(pt, h2f(vh[tt * kHeadDim + lane]), o0);
+    o1 = fmaf(pt, h2f(vh[tt * kHeadDim + lane + 64]), o1);
+  }
+  float* wp = ws + ((int64_t)(g * R + w) * T + tile) * (kHeadDim + 2);
+  if (lane == 0) {
+    wp[0] = m;
+    wp[1] = l;
+  }
+  wp[2 + lane] = o0;
+  wp[2 + 64 + lane] = o1;
+}
+
+// Combines the T partials of one query head (block h of NW waves): every wave
+// forms the maximum M of the tiles' maxima and the denominator sum_t l_t
+// exp(m_t - M) itself (the same fixed order in every wave); wave w adds
+// exp(m_t - M) o_t over its tiles t = w, w + NW, ... in order; the waves'
+// sums are added in wave order.  A wave's loads of a batch of 8 tiles are
+// issued before the statistics pass, so up to 8 * NW tiles cost one memory
+// round trip.
+template <int NW>
+__global__ __launch_bounds__(64 * NW) void attn_combine2_kernel(const float* __restrict__ ws, int T,
+                                                                uint16_t* __restrict__ out) {
+  __shared__ float num[NW][kHeadDim];
+  const int h = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const float* base = ws + (int64_t)h * T * (kHeadDim + 2);
+  // this wave's first batch of value sums, issued before the statistics
+  constexpr int kB = 8;
+  float a0[kB], a1[kB], mt[kB];
+#pragma unroll
+  for (int j = 0; j < kB; ++j) {
+    const int tt = min(w + NW * j, T - 1);
+    const float* pt = base + (int64_t)tt * (kHeadDim + 2);
+    mt[j] = pt[0];
+    a0[j] = pt[2 + lane];
+    a1[j] = pt[2 + 64 + lane];
+  }
+  float M = -INFINITY;
+  for (int t0 = 0; t0 < T; t0 += 64)
+    M = fmaxf(M, wave_max(t0 + lane < T ? base[(int64_t)(t0 + lane) * (kHeadDim + 2)] : -INFINITY));
+  float den = 0.0f;
+  for (int t0 = 0; t0 < T; t0 += 64) {
+    const int tt = t0 + lane;
+    const float* pt = base + (int64_t)min(tt, T - 1) * (kHeadDim + 2);
+    den += wave_sum(tt < T ? expf(pt[0] - M) * pt[1] : 0.0f);
+  }
+  float n0 = 0.0f, n1 = 0.0f;
+  for (int j0 = 0; w + NW * j0 < T; j0 += kB) {
+    if (j0 > 0) {
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        const int tt = min(w + NW * (j0 + j), T - 1);
+        const float* pt = base + (int64_t)tt * (kHeadDim + 2);
+        mt[j] = pt[0];
+        a0[j] = pt[2 + lane];
+        a1[j] = pt[2 + 64 + lane];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kB; ++j) {
+      const float e = (w + NW * (j0 + j) < T) ? expf(mt[j] - M) : 0.0f;
+      n0 = fmaf(e, a0[j], n0);
+      n1 = fmaf(e, a1[j], n1);
+    }
+  }
+  num[w][lane] = n0;
+  num[w][lane + 64] = n1;
+  __syncthreads();
+  if (w == 0) {
+    float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      s0 += num[i][lane];
+      s1 += num[i][lane + 64];
+    }
+    out[(int64_t)h * kHeadDim + lane] = f2h(s0 / den);
+    out[(int64_t)h * kHeadDim + lane + 64] = f2h(s1 / den);
+  }
+}
+
 // y[m][i] = silu(g) * u with g = gu[m][i], u = gu[m][I + i]; row m = blockIdx.y.
 __global__ __launch_bounds__(256) void silu_mul_kernel(const uint16_t* __restrict__ gu, uint16_t* __restrict__ y,
                                                        int64_t I) {
@@ -298,6 +506,53 @@ hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kc, const 
     default: launch(attn_partial_kernel<8>, grid, dim3(512), 0, stream, e1, q, kc, vc, S_max, (int)L, T, ws); break;
   }
   launch(attn_combine_kernel, dim3((unsigned)Hq), dim3(64), 0, stream, e2, (const float*)ws, T, out);
+  return hipGetLastError();
+}
+
+// Positions per tile of the fused attention: enough blocks (Hkv x tiles) to
+// give every compute unit work at short contexts, longer tiles (fewer
+// partials to combine) at long ones.
+int attention_qkv_tile(int64_t Hkv, int64_t L) {
+  const int64_t work = Hkv * L;
+  return work >= 32768 ? 64 : work >= 4096 ? 32 : 16;
+}
+
+int64_t decode_attention_qkv_tiles(int64_t Hkv, int64_t L) {
+  const int P = attention_qkv_tile(Hkv, L);
+  return (L + P - 1) / P;
+}
+
+hipError_t launch_decode_attention_qkv(const uint16_t* qkv, const uint16_t* qw, const uint16_t* kw,
+                                       const float* cos_sin, int64_t pos, int64_t Hq, int64_t Hkv, float eps,
+                                       uint16_t* kc, uint16_t* vc, int64_t S_max, uint16_t* out, float* ws,
+                                       hipStream_t stream, const LaunchEvents& ev) {
+  const int64_t L = pos + 1;
+  const int P = attention_qkv_tile(Hkv, L);
+  const int T = (int)((L + P - 1) / P);
+  const int R = (int)(Hq / Hkv);
+  LaunchEvents e1, e2;  // the measurement hook spans both kernels
+  e1.start = ev.start;
+  e2.stop = ev.stop;
+  const dim3 grid((unsigned)Hkv, (unsigned)T);
+  const float* cs = cos_sin + pos * kHeadDim;
+#define LAQ_ATTN_QKV(RV, PV)                                                                                 \
+  launch(attn_qkv_partial_kernel<RV, PV>, grid, dim3(64 * RV), 0, stream, e1, qkv, qw, kw, cs, eps, kc, vc, \
+         S_max, (int)pos, (int)Hq, (int)Hkv, T, ws)
+#define LAQ_ATTN_QKV_P(RV)                 \
+  do {                                     \
+    if (P == 64) LAQ_ATTN_QKV(RV, 64);     \
+    else if (P == 32) LAQ_ATTN_QKV(RV, 32); \
+    else LAQ_ATTN_QKV(RV, 16);             \
+  } while (0)
+  switch (R) {
+    case 1: LAQ_ATTN_QKV_P(1); break;
+    case 2: LAQ_ATTN_QKV_P(2); break;
+    case 4: LAQ_ATTN_QKV_P(4); break;
+    default: LAQ_ATTN_QKV_P(8); break;
+  }
+#undef LAQ_ATTN_QKV_P
+#undef LAQ_ATTN_QKV
+  launch(attn_combine2_kernel<4>, dim3((unsigned)Hq), dim3(256), 0, stream, e2, (const float*)ws, T, out);
   return hipGetLastError();
 }
 

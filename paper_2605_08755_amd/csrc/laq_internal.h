@@ -139,6 +139,11 @@ hipError_t launch_qk_norm_rope(const uint16_t* qkv, const uint16_t* qw, const ui
 hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, int64_t Hq,
                                    int64_t Hkv, int64_t L, int64_t S_max, uint16_t* out, float* ws,
                                    hipStream_t stream, const LaunchEvents& ev);
+int64_t decode_attention_qkv_tiles(int64_t Hkv, int64_t L);
+hipError_t launch_decode_attention_qkv(const uint16_t* qkv, const uint16_t* qw, const uint16_t* kw,
+                                       const float* cos_sin, int64_t pos, int64_t Hq, int64_t Hkv, float eps,
+                                       uint16_t* kc, uint16_t* vc, int64_t S_max, uint16_t* out, float* ws,
+                                       hipStream_t stream, const LaunchEvents& ev);
 hipError_t launch_silu_mul(const uint16_t* gu, uint16_t* y, int64_t M, int64_t I, hipStream_t stream,
                            const LaunchEvents& ev);
 

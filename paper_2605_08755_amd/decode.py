@@ -42,9 +42,13 @@ class DecodeStep:
     per layer (positions below the decoded one already filled).  lm_head:
     optional callable f(x, out) writing the logits out = x W^T (fp16
     [1][vocab], vocab = shape["vocab"]) from the final norm's output.
+    fused_attention: the per-head q/k norm, rotary embedding, cache append
+    and attention as laq.decode_attention_qkv (two kernels); False: the
+    separate laq.qk_norm_rope and laq.decode_attention calls (three).
     """
 
-    def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None):
+    def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None,
+                 fused_attention=True):
         import torch
         self.s = shape
         self.linears, self.norms, self.final_norm = linears, norms, final_norm
@@ -67,7 +71,10 @@ class DecodeStep:
         self.out = torch.empty((1, D), **f16)
         self.lm_head = lm_head
         self.logits = torch.empty((1, shape["vocab"]), **f16) if lm_head is not None else None
-        self.workspace = torch.empty(laq.attention_workspace_bytes(Hq, S_max), dtype=torch.uint8, device=device)
+        self.fused_attention = fused_attention
+        nbytes = (laq.attention_qkv_workspace_bytes(Hq, Hkv, S_max) if fused_attention
+                  else laq.attention_workspace_bytes(Hq, S_max))
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
 
     def run(self, pos):
         """Decode the token at position pos (attends to positions 0..pos).
@@ -81,10 +88,14 @@ class DecodeStep:
             w_in, w_post, qn, kn = self.norms[l]
             laq.add_rmsnorm(self.residual, delta, w_in, eps, out=self.h)
             f_qkv(self.h, self.qkv)
-            laq.qk_norm_rope(self.qkv, qn, kn, self.cos_sin, pos, Hq, Hkv, eps, self.k_caches[l], self.v_caches[l],
-                             q_out=self.q)
-            laq.decode_attention(self.q, self.k_caches[l], self.v_caches[l], pos + 1, out=self.attn,
-                                 workspace=self.workspace)
+            if self.fused_attention:
+                laq.decode_attention_qkv(self.qkv, qn, kn, self.cos_sin, pos, Hq, Hkv, eps, self.k_caches[l],
+                                         self.v_caches[l], out=self.attn, workspace=self.workspace)
+            else:
+                laq.qk_norm_rope(self.qkv, qn, kn, self.cos_sin, pos, Hq, Hkv, eps, self.k_caches[l],
+                                 self.v_caches[l], q_out=self.q)
+                laq.decode_attention(self.q, self.k_caches[l], self.v_caches[l], pos + 1, out=self.attn,
+                                     workspace=self.workspace)
             f_o(self.attn.view(1, Hq * HEAD_DIM), self.o)
             laq.add_rmsnorm(self.residual, self.o, w_post, eps, out=self.h)
             if getattr(f_gu, "swiglu", False):

@@ -29,7 +29,8 @@ EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profil
            "laq_linear_workspace_bytes", "laq_linear_ws_w3g128", "laq_linear_ws_w4g128",
            "laq_add_rmsnorm_f16", "laq_qk_norm_rope_f16", "laq_decode_attention_workspace_bytes",
            "laq_decode_attention_f16", "laq_silu_mul_f16", "laq_linear_swiglu_w3g128",
-           "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128")
+           "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128", "laq_decode_attention_qkv_workspace_bytes",
+           "laq_decode_attention_qkv_f16")
 HEAD_DIM = 128
 
 
@@ -77,7 +78,8 @@ def lib():
             f.argtypes = [ctypes.POINTER(LinearCall), ctypes.c_int32, I64, P]
             f.restype = ctypes.c_int32
         for name in ("laq_linear_w3g128", "laq_linear_w4g128", "laq_linear_swiglu_w3g128",
-                     "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128"):
+                     "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128", "laq_decode_attention_qkv_workspace_bytes",
+           "laq_decode_attention_qkv_f16"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, P, P, I64, I64, I64, P]
             f.restype = ctypes.c_int32
@@ -96,6 +98,10 @@ def lib():
         L.laq_decode_attention_workspace_bytes.restype = I64
         L.laq_decode_attention_f16.argtypes = [P, P, P, I64, I64, I64, I64, I64, P, P, I64, P]
         L.laq_decode_attention_f16.restype = ctypes.c_int32
+        L.laq_decode_attention_qkv_workspace_bytes.argtypes = [I64, I64, I64]
+        L.laq_decode_attention_qkv_workspace_bytes.restype = I64
+        L.laq_decode_attention_qkv_f16.argtypes = [P, P, P, P, I64, I64, I64, I64, F32, P, P, I64, P, P, I64, P]
+        L.laq_decode_attention_qkv_f16.restype = ctypes.c_int32
         L.laq_silu_mul_f16.argtypes = [P, P, I64, I64, P]
         L.laq_silu_mul_f16.restype = ctypes.c_int32
         _lib = L
@@ -335,6 +341,33 @@ def decode_attention(q, k_cache, v_cache, L, out=None, workspace=None):
     _check(lib().laq_decode_attention_f16(_ptr(q), _ptr(k_cache), _ptr(v_cache), Hq, Hkv, HEAD_DIM, int(L), S_max,
                                           _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                           _stream(q.device)))
+    return out
+
+
+def attention_qkv_workspace_bytes(Hq, Hkv, L):
+    return int(lib().laq_decode_attention_qkv_workspace_bytes(Hq, Hkv, L))
+
+
+def decode_attention_qkv(qkv, q_norm_weight, k_norm_weight, cos_sin, pos, Hq, Hkv, eps, k_cache, v_cache,
+                         out=None, workspace=None):
+    """qk_norm_rope + decode_attention over positions 0..pos in two kernels:
+    one token's q|k|v projection output -> attention output fp16 [Hq][128];
+    k and v written to row pos of the caches [Hkv][S_max][128]."""
+    import torch
+    assert qkv.is_cuda and qkv.dtype == torch.float16 and qkv.is_contiguous() and qkv.numel() == (Hq + 2 * Hkv) * HEAD_DIM
+    assert cos_sin.dtype == torch.float32 and cos_sin.dim() == 2 and cos_sin.shape[1] == HEAD_DIM and cos_sin.is_contiguous()
+    S_max = k_cache.shape[1]
+    assert k_cache.shape == (Hkv, S_max, HEAD_DIM) and v_cache.shape == k_cache.shape and cos_sin.shape[0] >= S_max
+    assert k_cache.dtype == torch.float16 and v_cache.dtype == torch.float16
+    if out is None:
+        out = torch.empty((Hq, HEAD_DIM), dtype=torch.float16, device=qkv.device)
+    need = attention_qkv_workspace_bytes(Hq, Hkv, pos + 1)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=qkv.device)
+    _check(lib().laq_decode_attention_qkv_f16(_ptr(qkv), _ptr(q_norm_weight), _ptr(k_norm_weight), _ptr(cos_sin),
+                                              int(pos), Hq, Hkv, HEAD_DIM, float(eps), _ptr(k_cache), _ptr(v_cache),
+                                              S_max, _ptr(out), _ptr(workspace),
+                                              workspace.numel() * workspace.element_size(), _stream(qkv.device)))
     return out
 
 

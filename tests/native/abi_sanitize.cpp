@@ -224,6 +224,36 @@ int main() {
   EXPECT(laq_decode_attention_f16(P, P, P, 32, 3, 128, 1024, 1024, P, P, ws, nullptr), LAQ_ERR_BAD_SHAPE, fn);
   EXPECT(laq_decode_attention_f16(P, P, P, 32, 8, 128, 1024, 1024, P, off(4), ws, nullptr), LAQ_ERR_MISALIGNED, fn);
 
+  fn = "laq_decode_attention_qkv_f16";
+  const int64_t wq = laq_decode_attention_qkv_workspace_bytes(32, 8, 1024);
+  EXPECT(laq_decode_attention_qkv_f16(nullptr, P, P, F, 10, 32, 8, 128, 1e-6f, P, P, 1024, P, P, wq, nullptr),
+         LAQ_ERR_NULL_POINTER, fn);
+  EXPECT(laq_decode_attention_qkv_f16(P, P, P, F, 10, 32, 8, 128, 1e-6f, P, P, 1024, P, nullptr, wq, nullptr),
+         LAQ_ERR_NULL_POINTER, fn);
+  for (int64_t pos : {(int64_t)-1, (int64_t)1024, kMax, kMin})
+    EXPECT(laq_decode_attention_qkv_f16(P, P, P, F, pos, 32, 8, 128, 1e-6f, P, P, 1024, P, P, wq, nullptr),
+           LAQ_ERR_BAD_SHAPE, fn);
+  EXPECT(laq_decode_attention_qkv_f16(P, P, P, F, 1023, 32, 8, 128, 1e-6f, P, P, 1024, P, P, wq - 1, nullptr),
+         LAQ_ERR_BAD_SHAPE, fn);
+  EXPECT(laq_decode_attention_qkv_f16(P, P, P, F, 10, 32, 8, 128, 1e-6f, P, P, 1024, P, P, kMin, nullptr),
+         LAQ_ERR_BAD_SHAPE, fn);
+  EXPECT(laq_decode_attention_qkv_f16(P, P, P, F, 10, 32, 8, 128, -1.0f, P, P, 1024, P, P, wq, nullptr),
+         LAQ_ERR_BAD_SHAPE, fn);
+  EXPECT(laq_decode_attention_qkv_f16(P, P, P, F, 10, 32, 8, 128, 1e-6f, P, off(8), 1024, P, P, wq, nullptr),
+         LAQ_ERR_MISALIGNED, fn);
+  for (int64_t h : hs)
+    for (int64_t kv : {kMin, (int64_t)-1, (int64_t)0, (int64_t)1, (int64_t)8, (int64_t)4096, kMax})
+      for (int64_t l : ls) {
+        const int64_t b = laq_decode_attention_qkv_workspace_bytes(h, kv, l);
+        ++g_checks;
+        const bool valid = h >= 1 && h <= 4096 && kv >= 1 && kv <= h && l >= 1 && l <= (1 << 21);
+        if (b < 0 || (valid != (b > 0))) {
+          std::printf("attention_qkv_workspace_bytes(%lld, %lld, %lld) = %lld\n", (long long)h, (long long)kv,
+                      (long long)l, (long long)b);
+          ++g_bad;
+        }
+      }
+
   fn = "laq_silu_mul_f16";
   EXPECT(laq_silu_mul_f16(nullptr, P, 1, 9728, nullptr), LAQ_ERR_NULL_POINTER, fn);
   for (int64_t m : {(int64_t)0, (int64_t)65536, kMax, kMin})

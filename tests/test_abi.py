@@ -302,3 +302,46 @@ def test_decode_ops_validation(L):
     assert f(ctypes.c_void_p(FAKE), ctypes.c_void_p(FAKE), 65536, 8, None) == laq.LAQ_ERR_BAD_SHAPE
     assert f(ctypes.c_void_p(FAKE + 1), ctypes.c_void_p(FAKE), 1, 8, None) == laq.LAQ_ERR_MISALIGNED
     assert b"laq_silu_mul_f16" in L.laq_last_error()
+
+
+def _attn_qkv(L, qkv=FAKE, qw=FAKE, kw=FAKE, cs=FAKE, pos=100, Hq=32, Hkv=8, hd=128, eps=1e-6, kc=FAKE, vc=FAKE,
+              S=1024, out=FAKE, ws=FAKE, wsb=1 << 24):
+    P = ctypes.c_void_p
+    return L.laq_decode_attention_qkv_f16(P(qkv), P(qw), P(kw), P(cs), pos, Hq, Hkv, hd, eps, P(kc), P(vc), S,
+                                          P(out), P(ws), wsb, None)
+
+
+def test_attention_qkv_validation(L):
+    for kw in ("qkv", "qw", "kw", "cs", "kc", "vc", "out", "ws"):
+        assert _attn_qkv(L, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _attn_qkv(L, hd=64) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn_qkv(L, Hq=24) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn_qkv(L, pos=1024) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn_qkv(L, pos=-1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn_qkv(L, eps=float("inf")) == laq.LAQ_ERR_BAD_SHAPE
+    need = L.laq_decode_attention_qkv_workspace_bytes(32, 8, 101)
+    assert _attn_qkv(L, wsb=need - 1) == laq.LAQ_ERR_BAD_SHAPE
+    assert _attn_qkv(L, ws=FAKE + 4) == laq.LAQ_ERR_MISALIGNED
+    assert _attn_qkv(L, kc=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_decode_attention_qkv_f16" in L.laq_last_error()
+
+
+def test_attention_qkv_workspace_bytes(L):
+    """Tiles of 16 positions while Hkv * L < 4096, 32 below 32768, then 64;
+    the query is the maximum over every context up to L, so a workspace
+    sized for S_max serves every decoded position."""
+    f = L.laq_decode_attention_qkv_workspace_bytes
+    per = 130 * 4
+    assert f(32, 8, 100) == 32 * 7 * per            # 100 positions in tiles of 16
+    assert f(32, 8, 511) == 32 * 32 * per           # 511 in tiles of 16 (32 tiles)
+    assert f(32, 8, 1024) == 32 * 32 * per          # 1024 in tiles of 32; 511 needed as many
+    assert f(32, 8, 4095) == 32 * 128 * per         # 4095 in tiles of 32
+    assert f(32, 8, 4096) == 32 * 128 * per         # 4096 in tiles of 64 (64 tiles) < 4095's 128
+    assert f(32, 8, 1 << 20) == 32 * (1 << 14) * per
+    for bad in ((0, 8, 10), (32, 0, 10), (32, 64, 10), (32, 8, 0), (32, 8, (1 << 21) + 1)):
+        assert f(*bad) == 0
+    prev = 0
+    for Lp in range(1, 5000, 7):  # nondecreasing in L
+        b = f(32, 8, Lp)
+        assert b >= prev
+        prev = b

@@ -93,6 +93,46 @@ def test_decode_attention(Hq, Hkv, L):
     assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
 
 
+@pytest.mark.parametrize("Hq,Hkv,pos,S", [(32, 8, 0, 64), (32, 8, 15, 64), (32, 8, 16, 64), (32, 8, 300, 1024),
+                                           (32, 8, 511, 1024), (32, 8, 512, 1024), (32, 8, 1023, 1024),
+                                           (32, 8, 4095, 4100), (32, 8, 4096, 4100), (8, 8, 63, 300),
+                                           (8, 8, 64, 300), (16, 8, 257, 300), (64, 8, 999, 1024),
+                                           (4, 2, 33, 40), (8, 1, 100, 128)])
+def test_decode_attention_qkv(Hq, Hkv, pos, S):
+    """laq_decode_attention_qkv_f16 (q/k RMSNorm + rotary embedding + cache
+    append + attention in one pass over the cache) against the oracle's
+    qk_norm_rope and attention (q rounded to fp16 as the separate call stores
+    it), across every tile length (16, 32, 64 positions), tile boundaries,
+    contexts of one position and query heads per key/value head of 1 to 8;
+    the cache rows other than pos stay untouched."""
+    say("decode_attention_qkv", Hq, Hkv, pos, S)
+    rng = np.random.default_rng(Hq * 1000 + pos)
+    qkv = f16(rng, (Hq + 2 * Hkv) * 128, 2.0)
+    qw = (1 + 0.2 * rng.standard_normal(128)).astype(np.float16)
+    kw = (1 + 0.2 * rng.standard_normal(128)).astype(np.float16)
+    cs = cos_sin_table(S)
+    Kc = f16(rng, (Hkv, S, 128))
+    Vc = f16(rng, (Hkv, S, 128))
+    kc, vc = dev(Kc), dev(Vc)
+    out = laq.decode_attention_qkv(dev(qkv), dev(qw), dev(kw), dev(cs), pos, Hq, Hkv, EPS, kc, vc)
+    torch.cuda.synchronize()
+    q_ref, k_ref, v_ref = OD.qk_norm_rope(qkv, qw, kw, pos, Hq, Hkv, 128, EPS, THETA)
+    kh, vh = kc.cpu().numpy(), vc.cpu().numpy()
+    r = linear_check(kh[:, pos], k_ref)
+    assert r["ok"], r
+    assert np.array_equal(vh[:, pos], v_ref.astype(np.float16))
+    others = np.arange(S) != pos
+    assert np.array_equal(kh[:, others], Kc[:, others]) and np.array_equal(vh[:, others], Vc[:, others])
+    ref = OD.decode_attention(q_ref.astype(np.float16), kh[:, :pos + 1], vh[:, :pos + 1])
+    r = linear_check(out.cpu().numpy(), ref)
+    assert r["ok"], r
+    # deterministic, and the caches' row pos rewritten with the same values
+    out2 = laq.decode_attention_qkv(dev(qkv), dev(qw), dev(kw), dev(cs), pos, Hq, Hkv, EPS, kc, vc)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16))
+    assert np.array_equal(kc.cpu().numpy(), kh) and np.array_equal(vc.cpu().numpy(), vh)
+
+
 @pytest.mark.parametrize("M,I", [(1, 9728), (2, 100), (1, 25600)])
 def test_silu_mul(M, I):
     say("silu_mul", M, I)
@@ -199,8 +239,8 @@ def _quantized(N, K, cfg, layer, proj, interleave_halves=False):
     return (codes, s, z), (dev(oracle.pack(codes, 3).view(np.int32)), dev(s.view(np.float16)), dev(z))
 
 
-@pytest.mark.parametrize("fused", [False, True])
-def test_decode_step_vs_oracle(fused):
+@pytest.mark.parametrize("fused,fused_attention", [(False, False), (True, True), (False, True)])
+def test_decode_step_vs_oracle(fused, fused_attention):
     """paper_2605_08755_amd.decode.DecodeStep over two Qwen3-4B-shaped layers
     plus an LM head (4096 vocabulary rows), W3 linears on oracle-quantized
     codes, at position 200 of a filled cache, against the oracle's
@@ -211,10 +251,13 @@ def test_decode_step_vs_oracle(fused):
     GPU's own fp16 input of that stage, within the linear tolerance (1e-3 x
     output RMS before the output's fp16 rounding; the fp32 residual stream
     to 1e-6 relative).  fused: the gate|up linear with SiLU-and-multiply in
-    its output stage.  Then the step (no recording) is captured in a HIP
-    graph: three replays, with eager steps between them, each give logits
-    bitwise equal to the checked eager step."""
-    say("decode step vs oracle, fused =", fused)
+    its output stage.  fused_attention: the q/k norm, rotary embedding, cache
+    append and attention in one call (the rotated q is then not materialized:
+    attention is checked against the oracle's q rounded to fp16).  Then the
+    step (no recording) is captured in a HIP graph: three replays, with eager
+    steps between them, each give logits bitwise equal to the checked eager
+    step."""
+    say("decode step vs oracle, fused =", fused, "fused attention =", fused_attention)
     from paper_2605_08755_amd import decode
     shape = dict(decode.QWEN3_4B, layers=2, vocab=4096)
     D, Hq, Hkv, I, S, V, pos = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256, 4096, 200
@@ -259,7 +302,8 @@ def test_decode_step_vs_oracle(fused):
 
     names = ("qkv", "o", "gu", "down")
     rec_lins = [tuple(recording(names[j], l, lins[l][j]) for j in range(4)) for l in range(2)]
-    step = decode.DecodeStep(shape, rec_lins, norms, dev(fin_h), kcs, vcs, DEV, lm_head=recording("lm", 2, lm))
+    step = decode.DecodeStep(shape, rec_lins, norms, dev(fin_h), kcs, vcs, DEV, lm_head=recording("lm", 2, lm),
+                             fused_attention=fused_attention)
     step.x0.copy_(dev(x0_h))
     logits = step.run(pos).clone()
     torch.cuda.synchronize()
@@ -284,14 +328,18 @@ def test_decode_step_vs_oracle(fused):
         check(("h", l), e_qkv["x"], OD.rmsnorm(e_qkv["res"], w_in, EPS))
         check(("qkv", l), e_qkv["out"], lin(e_qkv["x"], host[l]["qkv"]))
         q_ref, k_ref, v_ref = OD.qk_norm_rope(e_qkv["out"], qn, kn, pos, Hq, Hkv, 128, EPS, THETA)
-        check(("q", l), e_o["q"], q_ref)
+        if fused_attention:
+            q_att = q_ref.astype(np.float16)  # the rounding the fused call applies to q
+        else:
+            check(("q", l), e_o["q"], q_ref)
+            q_att = e_o["q"]
         kc, vc = kcs[l].cpu().numpy(), vcs[l].cpu().numpy()
         check(("k cache row", l), kc[:, pos], k_ref)
         assert np.array_equal(vc[:, pos], v_ref.astype(np.float16)), ("v cache row", l)
         others = np.arange(S) != pos
         assert np.array_equal(kc[:, others], kc_h[l][:, others]) and np.array_equal(vc[:, others], vc_h[l][:, others])
         check(("attention", l), e_o["x"].reshape(Hq, 128),
-              OD.decode_attention(e_o["q"], kc[:, :pos + 1], vc[:, :pos + 1]))
+              OD.decode_attention(q_att, kc[:, :pos + 1], vc[:, :pos + 1]))
         check(("o", l), e_o["out"], lin(e_o["x"], host[l]["o"]))
         assert np.allclose(e_gu["res"], e_o["res"].astype(np.float64) + e_o["out"].astype(np.float64),
                            rtol=1e-6, atol=1e-6), ("residual + o", l)
@@ -312,7 +360,8 @@ def test_decode_step_vs_oracle(fused):
     check("logits", logits.cpu().numpy(), lin(g[("lm", 2)]["x"], h_lm))
 
     # the same step without recording, captured in a HIP graph
-    gstep = decode.DecodeStep(shape, [tuple(f) for f in lins], norms, dev(fin_h), kcs, vcs, DEV, lm_head=lm)
+    gstep = decode.DecodeStep(shape, [tuple(f) for f in lins], norms, dev(fin_h), kcs, vcs, DEV, lm_head=lm,
+                              fused_attention=fused_attention)
     gstep.x0.copy_(dev(x0_h))
     eager = gstep.run(pos).clone()
     torch.cuda.synchronize()
