@@ -50,7 +50,7 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
 // Routing constants of the linear (measured on MI355X).  Every launch shape
 // is a pure function of (M, N, K) and these constants: the library keeps no
 // mutable state between calls.
-constexpr int kMfmaMinM = 3;               // activation rows from which the matrix-core path may be used
+constexpr int kMfmaMinM = 3;               // activation rows from which the matrix-core path is used
 constexpr int kResidentWaves = 8192;       // waves the chip keeps resident (256 compute units x 32)
 constexpr int kMfmaShareMinTiles = 1024;   // from this many 16-row tiles: tiles per block share the activations
 constexpr int kSplitMinQuads = 40;         // fewer tiles: K is split (given a workspace) from rows of this many quads

@@ -616,10 +616,8 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
                          size_t workspace_bytes) {
   const int G = (int)(K / 128);
   const int MT = ceil_pow2(M);
-  // Matrix cores from mfma_min_m rows on, except that the VALU kernel stays
-  // ahead up to 4 rows when rows are short (measured on MI355X: it re-reads
-  // the activations from LDS per unit, which costs more as rows get longer).
-  if (M >= kMfmaMinM && !(M <= 4 && G <= 24))
+  // Matrix cores from kMfmaMinM activation rows on.
+  if (M >= kMfmaMinM)
     return launch_linear_mfma<BITS>(x, qweight, scales, zeros, y, M, N, K, stream, ev, workspace, workspace_bytes);
   const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
@@ -782,7 +780,11 @@ hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t 
   int G_max = 1;
   for (int i = 0; i < count; ++i) G_max = max(G_max, calls[i].G);
   const int MT = ceil_pow2(M);
-  // Same routing as a single call, decided on the longest row of the group.
+  // Matrix cores from kMfmaMinM activation rows on, except that the VALU
+  // kernel stays ahead up to 4 rows when the group's rows are short (measured
+  // on MI355X: it re-reads the activations from LDS per unit, which costs more
+  // as rows get longer; the grouped matrix-core kernel has no one-wave-per-quad
+  // form).
   if (M >= kMfmaMinM && !(M <= 4 && G_max <= 24))
     return launch_linear_mfma_group<BITS>(calls, count, M, stream, ev);
   const int NT = G_max <= 32 ? 256 : (G_max <= 64 ? 512 : 1024);

@@ -716,6 +716,143 @@ __global__ __launch_bounds__(1024) void linear_mfma_group_kernel(const LinearGro
   mfma_block<BITS, 1>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, b - c.first_block);
 }
 
+// ---------------------------------------------------------------------------
+// One 16-row tile per block and one wave per quad (512 columns) of the row,
+// for rows of at most kQuadWaveMax quads whose activations fit in LDS.  Every
+// wave issues all its loads at once: its quad's activations
+// x[0..MT-1][512q, 512q+512) into its own LDS slab (direct-to-LDS; rows past M
+// and columns past K read zeros; no other wave reads it, so no barrier), then
+// the quad's weights (one register set).  It reads its sixteen A fragments
+// (4 groups x 4 MFMAs) from the slab as soon as the slab has arrived, then
+// multiplies by the weights, scales per group and writes its four
+// accumulators over its slab.  After one barrier the waves' partials are
+// added in wave order and rounded.  Compared with waves that each walk
+// several quads, every load of the tile is in flight at once and every wave
+// pays one memory round trip.
+// ---------------------------------------------------------------------------
+constexpr int kQuadWaveMax = 10;  // quads per row (waves per block) the kernel takes
+
+// ds_read_b128 at a register address plus a compile-time byte offset (inline
+// assembly for the reason given at lds_read_b128).
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_b128_off(uint32_t addr) {
+  u32x4 r;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
+template <int BITS, int MT>
+__global__ __launch_bounds__(64 * kQuadWaveMax) void linear_mfma_quad_wave_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
+  static_assert(MT == 4 || MT == 8 || MT == 16, "slab rows");
+  typedef __attribute__((address_space(3))) void lds_void;
+  extern __shared__ u32x4 wslab[];  // [W][MT rows][64 pieces]; afterwards [W][4][64] fp32 partials
+  constexpr int WL = BITS + 2;      // weight loads per lane
+  const int b = xcd_block();
+  if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
+  const int K = 128 * G;
+  const int W = (int)(blockDim.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // this wave's quad
+  const int nl = lane & 15;  // weight row / activation row / result column
+  const int j = lane >> 4;   // load: group of the quad; compute: chunk of the group
+  const int64_t row0 = (int64_t)b * 16;
+  const int rows = (int)min((int64_t)16, (int64_t)N - row0);
+  u32x4* const sl = wslab + wave * (MT * 64);
+
+  const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
+  const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * 4 * G, (uint32_t)rows * BITS * G * 16);
+  const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
+  const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
+
+  // 1. The slab (MT direct loads), then the weights.  The waits below count
+  //    outstanding loads in this issue order (scheduling barriers).
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    const int col = 512 * wave + 8 * (lane ^ (m & 7));
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sl + m * 64), 16,
+                                             (uint32_t)(m * K + col) * 2 | (uint32_t)!(m < M && col < K) << 31, 0,
+                                             0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  const QuadWeights<BITS> qwt = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, wave, G, true);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 2. The A fragments: group gi, MFMA jj reads piece 16 gi + 4 j + jj of the
+  //    lane's activation row (stored at position piece ^ (row & 7)).
+  wait_vmcnt<WL>();
+  __builtin_amdgcn_sched_barrier(0);
+  const int arow = nl & (MT - 1);
+  const uint32_t abase = lds_addr(sl + arow * 64);
+  const int swz = arow & 7;
+  uint32_t aoff[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) aoff[jj] = abase + 16 * ((4 * j + jj) ^ swz);
+  u32x4 af[4][4];
+  static_for<4>([&](auto gc) {
+    constexpr int gi = decltype(gc)::value;
+    static_for<4>([&](auto jc) {
+      constexpr int jj = decltype(jc)::value;
+      af[gi][jj] = lds_read_b128_off<256 * gi>(aoff[jj]);
+    });
+  });
+#pragma unroll
+  for (int gi = 0; gi < 4; ++gi) lds_wait(af[gi]);
+
+  // 3. Quarter transposes (chunk j of group 4q + gi in component gi), exact
+  //    (q - z) pairs, four MFMAs per group, scale.
+  wait_vmcnt<0>();
+  __builtin_amdgcn_sched_barrier(0);
+  uint32_t wt[BITS][4];
+#pragma unroll
+  for (int p = 0; p < BITS; ++p) {
+    wt[p][0] = qwt.w[p][0];
+    wt[p][1] = qwt.w[p][1];
+    wt[p][2] = qwt.w[p][2];
+    wt[p][3] = qwt.w[p][3];
+    transpose_quarters(wt[p][0], wt[p][1], wt[p][2], wt[p][3]);
+  }
+  uint32_t szj[4];
+  szj[0] = szj[1] = szj[2] = szj[3] = qwt.s | (qwt.z << 16);
+  transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
+  float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int gi = 0; gi < 4; ++gi) {
+    uint32_t w[BITS];
+#pragma unroll
+    for (int p = 0; p < BITS; ++p) w[p] = wt[p][gi];
+    uint32_t pr[16];
+    unpack_chunk_exact<BITS>(w, szj[gi] >> 16, pr);
+    float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const half8_t bf = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, af[gi][jj]), bf, c, 0, 0, 0);
+    }
+    const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[gi] & 0xFFFFu));
+    yacc += s * c;
+  }
+  float* part = reinterpret_cast<float*>(sl);  // [4][64], over the slab just read
+#pragma unroll
+  for (int r = 0; r < 4; ++r) part[r * 64 + lane] = yacc[r];
+  __syncthreads();
+
+  // 4. Outputs (row n, activation row m): the W waves' partials in order.
+  //    Lane (n, j) of a wave held rows m = 4j .. 4j+3 of column n.
+  const float* red = reinterpret_cast<const float*>(wslab);
+  const int wstride = MT * 64 * 4;  // floats per wave region
+  for (int idx = threadIdx.x; idx < 256; idx += blockDim.x) {
+    const int r = idx >> 6;
+    const int ln = idx & 63;
+    float v = 0.0f;
+    for (int w = 0; w < W; ++w) v += red[w * wstride + r * 64 + ln];
+    const int m = 4 * (ln >> 4) + r;
+    const int n = ln & 15;
+    if (m < M && n < rows) y[(int64_t)m * N + row0 + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+}
+
 }  // namespace
 
 SplitPlan mfma_split_plan(int M, int64_t N, int G) {
@@ -740,10 +877,27 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
                               size_t workspace_bytes) {
   const int G = (int)(K / 128);
   const int nq = (G + 3) / 4;
-  // Two tiles per block share each activation fragment when rows are long
-  // (the fragments then outweigh the weights) and there are enough tiles to
-  // keep a block on every compute unit (measured on MI355X).
   const int64_t tiles = (N + 15) / 16;
+  // Rows of at most kQuadWaveMax quads whose activation slabs fit in LDS: one
+  // tile per block, one wave per quad (measured on MI355X against the kernels
+  // below: faster for every Qwen3-4B projection from M = 3, except the
+  // gate|up call, over 1024 tiles, at M > 8).
+  {
+    const int MT = M <= 4 ? 4 : M <= 8 ? 8 : 16;
+    const size_t lds = (size_t)nq * MT * 1024;
+    if (nq <= kQuadWaveMax && lds <= (size_t)kBlockLdsU4 * 16 && (tiles < kMfmaShareMinTiles || M <= 8)) {
+      const int nblocks = (int)tiles;
+      const dim3 grid(xcd_grid(nblocks)), blk(64 * nq);
+#define LAQ_QW(MTV)                                                                                           \
+  launch(linear_mfma_quad_wave_kernel<BITS, MTV>, grid, blk, (uint32_t)lds, stream, ev, x, qweight, scales, zeros, \
+         y, M, (int)N, G, nblocks)
+      if (MT == 4) LAQ_QW(4);
+      else if (MT == 8) LAQ_QW(8);
+      else LAQ_QW(16);
+#undef LAQ_QW
+      return hipGetLastError();
+    }
+  }
   // Many tiles: blocks of four tiles share each activation slab through LDS.
   // Blocks of four tiles fit three to a compute unit (LDS), so up to 768
   // blocks are resident at once; from 3072 tiles on, blocks of eight (two to a
@@ -795,7 +949,10 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
            (const float*)workspace, y, sp.S, MN);
     return hipGetLastError();
   }
-  // (At most M tiles per wave: a wave's TW KiB of partials reuse its M KiB slab.)
+  // Two tiles per block share each activation fragment when rows are long
+  // (the fragments then outweigh the weights) and there are enough tiles to
+  // keep a block on every compute unit (measured on MI355X).  (At most M
+  // tiles per wave: a wave's TW KiB of partials reuse its M KiB slab.)
   const int TW = min(M, (tiles >= 256 && G >= 32) ? 2 : 1);
   // One wave per quad of the row, at most 8 (more waves per block measured
   // slower: Qwen3-4B down, 19 quads, at M = 16 10.3 us with 10 waves, 10.0

@@ -368,11 +368,36 @@ def test_max_k(bits):
         assert r["ok"], (M, r)
 
 
+QUAD_WAVE_SHAPES = [(17, 128), (300, 640), (1030, 2560), (257, 4992), (4100, 5120), (16400, 1152), (257, 5248)]
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("N,K", QUAD_WAVE_SHAPES)
+def test_matrix_core_quad_wave(bits, N, K):
+    """Rows of at most 10 quads: one 16-row tile per block, one wave per quad.
+    A single group (K = 128), a partial last quad (K = 640, five groups;
+    K = 4992, 39 groups, ten quads), ten full quads (K = 5120), a ragged last
+    tile (N = 17, 300, 1030, 257, 4100), at least 1024 tiles (N = 16400, the
+    kernel keeps them up to M = 8), and K = 5248 (eleven quads: just past the
+    kernel's limit).  M from 3 (four-row slab; rows of at most 24 groups
+    included) to 16 (sixteen-row slab)."""
+    say("mfma quad wave", bits, N, K)
+    w = inputs.weights(N, K, cfg=22, layer=bits, proj=K % 97)
+    codes, qw, s, z = oracle_packed(w, bits)
+    for M in (3, 4, 5, 8, 9, 16):
+        x = inputs.activations(M, K, cfg=22, layer=M)
+        y = gpu_linear(x, qw, s, z, bits)
+        r = linear_check(y, oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
+
+
 @pytest.mark.parametrize("bits", [3, 4])
 def test_matrix_core_two_tiles_ragged(bits):
-    """Enough 16-row tiles and long enough rows for blocks of two tiles,
-    with a last block holding a partial tile (N = 4100 = 128 * 32 + 4)."""
-    N, K = 4100, 4096
+    """Rows longer than 10 quads, enough 16-row tiles (>= 256) and long
+    enough rows for each wave to take two tiles, with a last block holding a
+    partial tile (N = 4100 = 256 * 16 + 4) and a partial last quad (K = 9728,
+    76 groups: 19 quads)."""
+    N, K = 4100, 9728
     say("mfma two tiles", bits, N, K)
     w = inputs.weights(N, K, cfg=16, layer=bits)
     codes, qw, s, z = oracle_packed(w, bits)
@@ -386,15 +411,16 @@ def test_matrix_core_two_tiles_ragged(bits):
 @pytest.mark.parametrize("bits", [3, 4])
 @pytest.mark.parametrize("N,K", [(16404, 640), (16400, 128), (16448, 2560)])
 def test_matrix_core_shared_slab(bits, N, K):
-    """Enough 16-row tiles (>= 1024) for blocks of four tiles sharing the
-    activation slabs through LDS (K <= 2560: all quads in one round trip): a
-    last block with a partial tile and idle waves (N = 16404 = 1025 * 16 + 4),
-    a partial last 4-group quad (K = 640, five groups) and a single group
-    (K = 128), and M from 2 to 16."""
+    """Enough 16-row tiles (>= 1024) and M > 8 for blocks of four tiles
+    sharing the activation slabs through LDS (K <= 2560: all quads in one
+    round trip): a last block with a partial tile and idle waves (N = 16404 =
+    1025 * 16 + 4), a partial last 4-group quad (K = 640, five groups) and a
+    single group (K = 128).  M = 2, 3 and 8 take the other kernels on the
+    same weights."""
     say("mfma shared slab", bits, N, K)
     w = inputs.weights(N, K, cfg=17, layer=bits, proj=K % 97)
     codes, qw, s, z = oracle_packed(w, bits)
-    for M in (2, 3, 5, 8, 16):
+    for M in (2, 3, 8, 9, 12, 16):
         x = inputs.activations(M, K, cfg=17, layer=M)
         y = gpu_linear(x, qw, s, z, bits)
         r = linear_check(y, oracle.linear(x, codes, s, z))
@@ -404,10 +430,12 @@ def test_matrix_core_shared_slab(bits, N, K):
 @pytest.mark.parametrize("bits", [3, 4])
 @pytest.mark.parametrize("K", [3072, 4096])
 def test_matrix_core_walk_four_tiles(bits, K):
-    """1024..3071 row tiles walk K in blocks of four tiles, the quad weights
-    in three register sets in turn: K = 3072 (6 quads, the unrolled loop
-    ends exactly) and 4096 (8 quads, two quads after the loop); N = 16400 =
-    1025 * 16 (a last block with one tile).  Sampled rows and the last rows."""
+    """1024..3071 row tiles at M > 8 walk K in blocks of four tiles, the quad
+    weights in three register sets in turn: K = 3072 (6 quads, the unrolled
+    loop ends exactly) and 4096 (8 quads, two quads after the loop); N =
+    16400 = 1025 * 16 (a last block with one tile).  M = 3 takes the
+    one-wave-per-quad kernel on the same weights.  Sampled rows and the last
+    rows."""
     N = 16400
     say("mfma walk four tiles", bits, N, K)
     rng = np.random.default_rng(K + bits)
@@ -419,7 +447,7 @@ def test_matrix_core_walk_four_tiles(bits, K):
     del wd
     torch.cuda.synchronize()
     assert np.array_equal(q[rows].cpu().numpy().view(np.uint32), qw)
-    for M in (3, 16):
+    for M in (3, 12, 16):
         x = inputs.activations(M, K, cfg=19, layer=M)
         y = laq.linear(to_dev(x), q, sd, zd, bits)
         torch.cuda.synchronize()
@@ -430,10 +458,10 @@ def test_matrix_core_walk_four_tiles(bits, K):
 
 @pytest.mark.parametrize("M", [3, 5])
 def test_matrix_core_two_tiles_per_wave_small_m(M):
-    """Fewer than 1024 tiles, at least 256 of them and rows of 32 groups or
-    more: each wave takes two tiles, and its two KiB of partials reuse an
-    activation slab of only M rows.  N = 4100 (ragged), K = 4096."""
-    N, K = 4100, 4096
+    """Fewer than 1024 tiles, at least 256 of them and rows of more than 10
+    quads: each wave takes two tiles, and its two KiB of partials reuse an
+    activation slab of only M rows.  N = 4100 (ragged), K = 6144 (12 quads)."""
+    N, K = 4100, 6144
     say("mfma two tiles per wave", M, N, K)
     w = inputs.weights(N, K, cfg=20, layer=M)
     x = inputs.activations(M, K, cfg=20, layer=M)
@@ -444,10 +472,11 @@ def test_matrix_core_two_tiles_per_wave_small_m(M):
 
 
 def test_matrix_core_walk_ragged():
-    """From 3072 row tiles, blocks of eight tiles walk K one quad at a time
-    (K > 2560): N = 49168 = 3073 * 16 (a last block with one tile), K = 3200
-    (25 groups: a partial last quad).  Quantize on the GPU; codes and outputs
-    checked on sampled rows and the last rows."""
+    """From 3072 row tiles at M > 8, blocks of eight tiles walk K one quad at
+    a time (K > 2560): N = 49168 = 3073 * 16 (a last block with one tile),
+    K = 3200 (25 groups: a partial last quad).  M = 3 and 8 take the
+    one-wave-per-quad kernel on the same weights.  Quantize on the GPU; codes
+    and outputs checked on sampled rows and the last rows."""
     N, K = 49168, 3200
     say("mfma walk ragged", N, K)
     rng = np.random.default_rng(49)
@@ -459,7 +488,7 @@ def test_matrix_core_walk_ragged():
     del wd
     torch.cuda.synchronize()
     assert np.array_equal(q[rows].cpu().numpy().view(np.uint32), qw)
-    for M in (3, 8, 16):
+    for M in (3, 8, 11, 16):
         x = inputs.activations(M, K, cfg=18, layer=M)
         y = laq.linear(to_dev(x), q, sd, zd, 3)
         torch.cuda.synchronize()
@@ -548,13 +577,16 @@ def _group_case(bits, specs, M, cfg):
 @pytest.mark.parametrize("bits", [3, 4])
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 8, 16])
 def test_group_qkv(bits, M):
-    """q, k, v of a Qwen3-4B layer (same activations) as one launch."""
+    """q, k, v of a Qwen3-4B layer (same activations) as one launch.  Up to
+    M = 2 the grouped and the single calls run the same VALU kernel body and
+    agree bit for bit; at M = 3 and 4 the group stays on the VALU kernel
+    (its rows are short) while a single call takes the matrix cores."""
     say("group qkv", bits, M)
     ys, singles, refs = _group_case(bits, [(4096, 2560, 0), (1024, 2560, 0), (1024, 2560, 0)], M, cfg=40)
     for y, y1, ref in zip(ys, singles, refs):
         r = linear_check(y, ref)
         assert r["ok"], r
-        if M <= 4:  # one-row VALU path: the same kernel body, bit for bit
+        if M <= 2:  # the same kernel body, bit for bit
             assert np.array_equal(y.view(np.uint16), y1.view(np.uint16))
 
 
@@ -590,9 +622,11 @@ def test_group_long_rows_one_row(bits):
 # ---------------------------------------------------------------------------
 GRAPH_CASES = [
     ("flat M=2 two rows per lane", 2, 300, 9728, 3),
-    ("matrix cores one tile M=5", 5, 1030, 4096, 4),
+    ("matrix cores one wave per quad M=5", 5, 1030, 4096, 4),
+    ("matrix cores one wave per quad M=16", 16, 300, 5120, 3),
+    ("matrix cores one tile M=5", 5, 1030, 9728, 4),
     ("matrix cores four tiles M=16", 16, 16400, 2560, 3),
-    ("matrix cores walk M=8", 8, 16400, 4096, 3),
+    ("matrix cores walk M=12", 12, 16400, 4096, 3),
     ("split K with workspace M=16", 16, 1030, 25600, 3),
 ]
 
