@@ -368,7 +368,8 @@ def test_max_k(bits):
         assert r["ok"], (M, r)
 
 
-QUAD_WAVE_SHAPES = [(17, 128), (300, 640), (1030, 2560), (257, 4992), (4100, 5120), (16400, 1152), (257, 5248)]
+QUAD_WAVE_SHAPES = [(17, 128), (300, 640), (1030, 2560), (257, 4992), (4100, 5120), (16400, 1152), (10256, 4992),
+                    (257, 5248)]
 
 
 @pytest.mark.parametrize("bits", [3, 4])
@@ -378,8 +379,10 @@ def test_matrix_core_quad_wave(bits, N, K):
     A single group (K = 128), a partial last quad (K = 640, five groups;
     K = 4992, 39 groups, ten quads), ten full quads (K = 5120), a ragged last
     tile (N = 17, 300, 1030, 257, 4100), at least 1024 tiles (N = 16400, the
-    kernel keeps them up to M = 8), and K = 5248 (eleven quads: just past the
-    kernel's limit).  M from 3 (four-row slab; rows of at most 24 groups
+    kernel keeps them up to M = 8), more waves than stay resident with the
+    fragments read up front (N = 10256, K = 4992: 641 tiles x 10 waves, the
+    64-register form), and K = 5248 (eleven quads: just past the kernel's
+    limit).  M from 3 (four-row slab; rows of at most 24 groups
     included) to 16 (sixteen-row slab)."""
     say("mfma quad wave", bits, N, K)
     w = inputs.weights(N, K, cfg=22, layer=bits, proj=K % 97)
@@ -624,6 +627,7 @@ GRAPH_CASES = [
     ("flat M=2 two rows per lane", 2, 300, 9728, 3),
     ("matrix cores one wave per quad M=5", 5, 1030, 4096, 4),
     ("matrix cores one wave per quad M=16", 16, 300, 5120, 3),
+    ("matrix cores one wave per quad, 64 registers M=4", 4, 10256, 4992, 3),
     ("matrix cores one tile M=5", 5, 1030, 9728, 4),
     ("matrix cores four tiles M=16", 16, 16400, 2560, 3),
     ("matrix cores walk M=12", 12, 16400, 4096, 3),
