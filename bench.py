@@ -265,9 +265,10 @@ def decode_step_extra(stack, dev, steps, context=1024):
     positions, SiLU-and-multiply, the stack's linears, the final norm and the
     LM head over Qwen3-4B's 151936-token vocabulary), the token at position
     context - 1, captured in a HIP graph.  Variants: W3 linears and a W3 LM
-    head; W3 with the gate|up + SiLU linear and a W3 or an fp16 LM head; fp16
-    weights everywhere through torch's dense GEMM (the unquantized
-    reference).  The paper does not say whether its decoding benchmark
+    head; W3 with the gate|up + SiLU linear and a W3 or an fp16 LM head; the
+    same with the norms before q|k|v and gate|up inside those linears
+    (laq.add_rmsnorm_linear); fp16 weights everywhere through torch's dense
+    GEMM (the unquantized reference).  The paper does not say whether its decoding benchmark
     quantizes the LM head, hence both heads.  Attention is the fused
     q/k-norm + rotary + attention call except in the _separate_attention
     variant (qk-norm-rope, attention partials, combine: three kernels)."""
@@ -309,10 +310,26 @@ def decode_step_extra(stack, dev, steps, context=1024):
         f.swiglu = True
         return f
 
+    def with_norm(f, q, sc, z, swiglu=False):
+        # the norm before this linear computed inside it (laq.add_rmsnorm_linear)
+        f.norm_linear = lambda res, delta, w, eps, res_out, out: laq.add_rmsnorm_linear(
+            res, delta, w, eps, q, sc, z, 3, swiglu=swiglu, out=out, residual_out=res_out)
+        return f
+
+    def w3_norm_lin(i):
+        if i % 4 == 2:
+            f = w3_swiglu_lin(i)
+            return with_norm(f, *swiglu_w[i], swiglu=True)
+        f = w3_lin(i)
+        return with_norm(f, *stack.q[3][i]) if i % 4 == 0 else f
+
+    # (the final norm stays a separate call: inside the 151936-row head's
+    # 6331 blocks the prologue costs more than the norm's own launch)
     head_w3 = lambda x, out: laq.linear(x, *q_head, 3, out=out)
     head_fp16 = lambda x, out: torch.mm(x, w_head.t(), out=out)
     out = {"context": context, "layers": shape["layers"], "vocab": V}
     variants = (("w3", w3_lin, head_w3, True), ("w3_fused_swiglu", w3_swiglu_lin, head_w3, True),
+                ("w3_fused_swiglu_fused_norms", w3_norm_lin, head_w3, True),
                 ("w3_fused_swiglu_separate_attention", w3_swiglu_lin, head_w3, False),
                 ("w3_fused_swiglu_fp16_head", w3_swiglu_lin, head_fp16, True), ("fp16", fp16_lin, head_fp16, True))
     for name, mk, head, fused_attention in variants:
@@ -324,7 +341,7 @@ def decode_step_extra(stack, dev, steps, context=1024):
         out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}
         del step
     swiglu_w.clear()
-    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fp16_head"):
+    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fused_norms", "w3_fused_swiglu_fp16_head"):
         out[name + "_speedup_vs_fp16"] = round(out["fp16"]["us"] / out[name]["us"], 3)
     return out
 

@@ -321,6 +321,53 @@ laq_status laq_linear_swiglu_w4g128(const void *x, const uint32_t *qweight,
  * no allocation; outputs must not alias inputs unless stated.
  * ------------------------------------------------------------------------ */
 
+/* laq_add_rmsnorm_linear_w3g128 -- laq_add_rmsnorm_f16 for one token (M = 1,
+ * D = K) followed by laq_linear_w3g128 on its output, in one kernel: every
+ * block of the linear forms
+ *   r = residual + delta;  x = fp16(r / sqrt(mean(r^2) + eps) * norm_weight)
+ * itself while it stages its activation row (the decode step's norms before
+ * the attention and before the MLP feed a linear; Sec. 5, Table 3 setting),
+ * and y = x w_hat^T as laq_linear_w3g128 (Eq. 1 dequantization, App. H
+ * format).  The normalized row is not written.
+ *   residual      [in] fp32 [K], 16-byte aligned.
+ *   delta         [in] fp16 [K], 16-byte aligned, or NULL (then r = residual).
+ *   norm_weight   [in] fp16 [K], 16-byte aligned.
+ *   residual_out  [out] fp32 [K], 16-byte aligned, receives r; or NULL.  Must
+ *                 not overlap residual (the blocks read residual while one of
+ *                 them writes r).
+ *   qweight, scales, zeros, y, N  as laq_linear_w3g128 with M = 1.
+ * Results: y within the linear's tolerance of the two-call sequence (the
+ * sum of squares is added in another order; x can differ by one fp16 ulp),
+ * r bitwise equal to laq_add_rmsnorm_f16's residual; deterministic.
+ * Errors: NULL_POINTER (residual, norm_weight, qweight, scales, zeros, y);
+ * BAD_SHAPE (N < 1, K not a multiple of 128, K > 8192, eps < 0 or not finite,
+ * residual_out overlapping residual); MISALIGNED. */
+laq_status laq_add_rmsnorm_linear_w3g128(const float *residual, const void *delta, const void *norm_weight,
+                                         float eps, float *residual_out, const uint32_t *qweight,
+                                         const void *scales, const uint8_t *zeros, void *y, int64_t N,
+                                         int64_t K, void *stream);
+
+/* laq_add_rmsnorm_linear_swiglu_w3g128 -- the same prologue followed by
+ * laq_linear_swiglu_w3g128 (gate and up rows interleaved, N even, y fp16
+ * [N/2] = silu(gate) * up). */
+laq_status laq_add_rmsnorm_linear_swiglu_w3g128(const float *residual, const void *delta,
+                                                const void *norm_weight, float eps, float *residual_out,
+                                                const uint32_t *qweight, const void *scales,
+                                                const uint8_t *zeros, void *y, int64_t N, int64_t K,
+                                                void *stream);
+
+/* W4G128 siblings of the two calls above (qweight as laq_linear_w4g128). */
+laq_status laq_add_rmsnorm_linear_w4g128(const float *residual, const void *delta, const void *norm_weight,
+                                         float eps, float *residual_out, const uint32_t *qweight,
+                                         const void *scales, const uint8_t *zeros, void *y, int64_t N,
+                                         int64_t K, void *stream);
+
+laq_status laq_add_rmsnorm_linear_swiglu_w4g128(const float *residual, const void *delta,
+                                                const void *norm_weight, float eps, float *residual_out,
+                                                const uint32_t *qweight, const void *scales,
+                                                const uint8_t *zeros, void *y, int64_t N, int64_t K,
+                                                void *stream);
+
 /* laq_add_rmsnorm_f16 -- residual update and RMSNorm, row by row:
  *   r = residual + delta;  y = fp16(r / sqrt(mean(r^2) + eps) * weight)
  *   residual  [in/out] fp32 [M][D]; receives r (may be read by later calls).

@@ -369,6 +369,35 @@ laq_status linear_swiglu(const char* fn, const void* x, const uint32_t* qweight,
                                                         static_cast<hipStream_t>(stream), ev));
 }
 
+template <int BITS>
+laq_status norm_linear(const char* fn, const float* residual, const void* delta, const void* norm_weight, float eps,
+                       float* residual_out, const uint32_t* qweight, const void* scales, const uint8_t* zeros,
+                       void* y, int64_t N, int64_t K, bool swiglu, void* stream) {
+  const laq::LaunchEvents ev = take_events();
+  if (!residual || !norm_weight || !qweight || !scales || !zeros || !y)
+    return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (!laq::norm_linear_fits(K)) return fail(LAQ_ERR_BAD_SHAPE, fn, "need K <= 8192");
+  if (swiglu && N % 2 != 0) return fail(LAQ_ERR_BAD_SHAPE, fn, "N (gate and up rows interleaved) must be even");
+  if (!(eps >= 0.0f) || !(eps < INFINITY)) return fail(LAQ_ERR_BAD_SHAPE, fn, "eps must be finite and >= 0");
+  if (residual_out != nullptr && residual_out < residual + K && residual < residual_out + K)
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "residual_out must not overlap residual");
+  if (!aligned(residual, 16) || !aligned(delta, 16) || !aligned(norm_weight, 16) || !aligned(residual_out, 16) ||
+      !aligned(qweight, 16))
+    return fail(LAQ_ERR_MISALIGNED, fn, "residual, residual_out, delta, norm_weight and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  laq::NormPrologue np;
+  np.res_in = residual;
+  np.delta = static_cast<const uint16_t*>(delta);
+  np.weight = static_cast<const uint16_t*>(norm_weight);
+  np.res_out = residual_out;
+  np.eps = eps;
+  return hip_status(fn, laq::launch_linear_norm<BITS>(np, qweight, static_cast<const uint16_t*>(scales), zeros,
+                                                      static_cast<uint16_t*>(y), N, K, swiglu,
+                                                      static_cast<hipStream_t>(stream), ev));
+}
+
 }  // namespace
 
 extern "C" {
@@ -381,6 +410,36 @@ laq_status laq_linear_swiglu_w3g128(const void* x, const uint32_t* qweight, cons
 laq_status laq_linear_swiglu_w4g128(const void* x, const uint32_t* qweight, const void* scales,
                                     const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {
   return linear_swiglu<4>("laq_linear_swiglu_w4g128", x, qweight, scales, zeros, y, M, N, K, stream);
+}
+
+laq_status laq_add_rmsnorm_linear_w3g128(const float* residual, const void* delta, const void* norm_weight, float eps,
+                                         float* residual_out, const uint32_t* qweight, const void* scales,
+                                         const uint8_t* zeros, void* y, int64_t N, int64_t K, void* stream) {
+  return norm_linear<3>("laq_add_rmsnorm_linear_w3g128", residual, delta, norm_weight, eps, residual_out, qweight,
+                        scales, zeros, y, N, K, false, stream);
+}
+
+laq_status laq_add_rmsnorm_linear_w4g128(const float* residual, const void* delta, const void* norm_weight, float eps,
+                                         float* residual_out, const uint32_t* qweight, const void* scales,
+                                         const uint8_t* zeros, void* y, int64_t N, int64_t K, void* stream) {
+  return norm_linear<4>("laq_add_rmsnorm_linear_w4g128", residual, delta, norm_weight, eps, residual_out, qweight,
+                        scales, zeros, y, N, K, false, stream);
+}
+
+laq_status laq_add_rmsnorm_linear_swiglu_w3g128(const float* residual, const void* delta, const void* norm_weight,
+                                                float eps, float* residual_out, const uint32_t* qweight,
+                                                const void* scales, const uint8_t* zeros, void* y, int64_t N,
+                                                int64_t K, void* stream) {
+  return norm_linear<3>("laq_add_rmsnorm_linear_swiglu_w3g128", residual, delta, norm_weight, eps, residual_out,
+                        qweight, scales, zeros, y, N, K, true, stream);
+}
+
+laq_status laq_add_rmsnorm_linear_swiglu_w4g128(const float* residual, const void* delta, const void* norm_weight,
+                                                float eps, float* residual_out, const uint32_t* qweight,
+                                                const void* scales, const uint8_t* zeros, void* y, int64_t N,
+                                                int64_t K, void* stream) {
+  return norm_linear<4>("laq_add_rmsnorm_linear_swiglu_w4g128", residual, delta, norm_weight, eps, residual_out,
+                        qweight, scales, zeros, y, N, K, true, stream);
 }
 
 laq_status laq_silu_mul_f16(const void* gate_up, void* y, int64_t M, int64_t I, void* stream) {

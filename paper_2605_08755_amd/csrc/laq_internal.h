@@ -47,6 +47,17 @@ inline void launch(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st
     hipLaunchKernelGGL(kernel, grid, block, lds, stream, args...);
 }
 
+// Residual add + RMSNorm that a batch-1 linear applies to its activation row
+// while staging it (the decode step's pre-attention and pre-MLP norms):
+// v = res_in + delta (fp32), x = fp16(v / sqrt(mean(v^2) + eps) * weight).
+struct NormPrologue {
+  const float* res_in = nullptr;     // [K] fp32 residual stream
+  const uint16_t* delta = nullptr;   // [K] fp16 added to it, or nullptr
+  const uint16_t* weight = nullptr;  // [K] fp16 RMSNorm weight
+  float* res_out = nullptr;          // [K] v, written by one block, or nullptr; never res_in
+  float eps = 0.0f;
+};
+
 // Routing constants of the linear (measured on MI355X).  Every launch shape
 // is a pure function of (M, N, K) and these constants: the library keeps no
 // mutable state between calls.
@@ -128,6 +139,15 @@ template <int BITS>
 hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                                 const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K, hipStream_t stream,
                                 const LaunchEvents& ev);
+
+// Batch-1 linear (gate|up + SiLU-and-multiply when swiglu) whose activation
+// row is the residual add + RMSNorm of np, computed while the row is staged.
+// Shapes: norm_linear_fits(K); N even when swiglu.
+bool norm_linear_fits(int64_t K);
+template <int BITS>
+hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, const uint16_t* scales,
+                              const uint8_t* zeros, uint16_t* y, int64_t N, int64_t K, bool swiglu,
+                              hipStream_t stream, const LaunchEvents& ev);
 
 // Decode-step operations (decode.hip); head dimension 128.
 int64_t decode_attention_tiles(int64_t L);

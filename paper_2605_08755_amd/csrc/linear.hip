@@ -266,6 +266,104 @@ __device__ __forceinline__ void stage_x_pass(const u32x4 (&xv)[XB], int base, in
   }
 }
 
+// Sum over the 64 lanes of a wave in a fixed order (every lane receives it):
+// DPP sums of the four 16-lane rows, then the rows in order (lane reads; no
+// LDS round trips).
+__device__ __forceinline__ float wave_sum64(float v) {
+  v = row16_sum(v);
+  const int b = __builtin_bit_cast(int, v);
+  return ((__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0)) +
+           __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16))) +
+          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32))) +
+         __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48));
+}
+
+// Norm prologue, loads: this thread's activation units t + i*NT (8 values
+// each) of the residual, the delta and the norm weight.  Units past the row
+// (and the delta when there is none) read zeros.
+template <int XB>
+struct NormLoads {
+  u32x4 r0[XB], r1[XB], d[XB], w[XB];
+};
+
+template <int XB, int NT>
+__device__ __forceinline__ NormLoads<XB> norm_issue(const NormPrologue& np, int K, int t) {
+  NormLoads<XB> L;
+  const __amdgpu_buffer_rsrc_t rr = make_rsrc(np.res_in, (uint32_t)K * 4);
+  const __amdgpu_buffer_rsrc_t dr = make_rsrc(np.delta, np.delta ? (uint32_t)K * 2 : 0u);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(np.weight, (uint32_t)K * 2);
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    const uint32_t u = (uint32_t)(t + i * NT);
+    L.r0[i] = __builtin_amdgcn_raw_buffer_load_b128(rr, u * 32, 0, 0);
+    L.r1[i] = __builtin_amdgcn_raw_buffer_load_b128(rr, u * 32 + 16, 0, 0);
+    L.d[i] = __builtin_amdgcn_raw_buffer_load_b128(dr, u * 16, 0, 0);
+    L.w[i] = __builtin_amdgcn_raw_buffer_load_b128(wr, u * 16, 0, 0);
+  }
+  return L;
+}
+
+__device__ __forceinline__ float u2f(uint32_t u) { return __builtin_bit_cast(float, u); }
+__device__ __forceinline__ float lo_h(uint32_t u) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(u & 0xFFFFu)); }
+__device__ __forceinline__ float hi_h(uint32_t u) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(u >> 16)); }
+__device__ __forceinline__ uint32_t pack_h2(float a, float b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)a) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)b) << 16);
+}
+
+// Norm prologue, arithmetic: v = res + delta, the row's sum of squares over
+// the block (thread partials in unit order, wave sums, waves in order),
+// x = fp16(v / sqrt(mean(v^2) + eps) * weight) into xv (the activation units
+// the staging pass writes to LDS).  The writer block stores v to res_out.
+// Every thread of the block calls it (one barrier).  The whole row is this
+// thread's XB units: K <= 8 * XB * NT.
+template <int XB, int NT>
+__device__ __forceinline__ void norm_finish(const NormLoads<XB>& L, const NormPrologue& np, int K, int t,
+                                            bool writer, u32x4 (&xv)[XB]) {
+  __shared__ float red[NT / 64];
+  float v[XB][8];
+  float ss = 0.0f;
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    // (elements are copied to scalars first: a bit cast of a vector element
+    // expression was compiled as a cast of element 0)
+    const float r[8] = {u2f(L.r0[i].x), u2f(L.r0[i].y), u2f(L.r0[i].z), u2f(L.r0[i].w),
+                        u2f(L.r1[i].x), u2f(L.r1[i].y), u2f(L.r1[i].z), u2f(L.r1[i].w)};
+    const uint32_t d[4] = {L.d[i].x, L.d[i].y, L.d[i].z, L.d[i].w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[i][e] = r[e] + ((e & 1) ? hi_h(d[e >> 1]) : lo_h(d[e >> 1]));
+      ss = fmaf(v[i][e], v[i][e], ss);
+    }
+  }
+  ss = wave_sum64(ss);
+  if ((t & 63) == 0) red[t >> 6] = ss;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)K + np.eps);
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    const uint32_t w[4] = {L.w[i].x, L.w[i].y, L.w[i].z, L.w[i].w};
+    uint32_t x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      x[e] = pack_h2(v[i][2 * e] * inv * lo_h(w[e]), v[i][2 * e + 1] * inv * hi_h(w[e]));
+    xv[i] = u32x4{x[0], x[1], x[2], x[3]};
+  }
+  if (writer && np.res_out != nullptr) {
+#pragma unroll
+    for (int i = 0; i < XB; ++i) {
+      const int u = t + i * NT;
+      if (8 * u < K) {
+        float4* o = reinterpret_cast<float4*>(np.res_out + 8 * u);
+        o[0] = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
+        o[1] = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
+      }
+    }
+  }
+}
+
 // Dot products of RPL units that share group g (rows of one lane): the
 // group's activations are read from LDS once per chunk and used for every
 // row, so LDS reads per weight fall by RPL.
@@ -331,11 +429,11 @@ __device__ __forceinline__ void swiglu_rows(const float* part, int R, int G, int
 // Thread t takes units t + i*NT (i < UPT) of each pass over the block's
 // units; every launch uses UPT = 1 (more units per thread measured slower).
 // SW: the fused gate|up + SiLU-and-multiply output stage (swiglu_rows).
-template <int BITS, int MT, int NT, int UPT, int XB, bool SW = false>
+template <int BITS, int MT, int NT, int UPT, int XB, bool SW = false, bool NORM = false>
 __device__ __forceinline__ void flat_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int block) {
+    int block, const NormPrologue& np = NormPrologue{}) {
   extern __shared__ u32x4 lds[];
   u32x4* xl = lds;                                                                // [MT][G][17]
   float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
@@ -371,9 +469,14 @@ __device__ __forceinline__ void flat_block(
   //    the weight stream wait for an activation round trip.
   //    Index XM = M*G*16 is the end of x's extent: loads past it read zero.
   u32x4 xv[XB];
+  NormLoads<NORM ? XB : 1> nl_;  // the norm prologue's loads (NORM: the row's residual, delta, weight)
+  if constexpr (NORM) {
+    nl_ = norm_issue<XB, NT>(np, 128 * G, t);
+  } else {
 #pragma unroll
-  for (int i = 0; i < XB; ++i)
-    xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
+    for (int i = 0; i < XB; ++i)
+      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
+  }
   u32x4 wv[UPT][BITS];
   float sv[UPT], zv[UPT];
   int gi[UPT];
@@ -391,8 +494,9 @@ __device__ __forceinline__ void flat_block(
   __builtin_amdgcn_sched_barrier(0);
 
   // 3. Stage activations and per-group sums (first pass from the loads above).
+  if constexpr (NORM) norm_finish<XB, NT>(nl_, np, 128 * G, t, block == 0, xv);
   stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);
-  for (int base = XB * NT; base < XU; base += XB * NT) {
+  for (int base = XB * NT; !NORM && base < XU; base += XB * NT) {
 #pragma unroll
     for (int i = 0; i < XB; ++i)
       xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(base + t + i * NT) * 16, 0, 0);
@@ -482,11 +586,11 @@ __device__ __forceinline__ void flat_block(
 // form RPL layers of R1 = R / RPL rows (R1 * G <= NT), and thread
 // t = r*G + g of the first layer takes group g of rows r, r + R1, r + 2*R1,
 // ...  Loads, staging and the row sums are those of flat_block.
-template <int BITS, int MT, int NT, int RPL, int XB, bool SW = false>
+template <int BITS, int MT, int NT, int RPL, int XB, bool SW = false, bool NORM = false>
 __device__ __forceinline__ void flat_block_rpl(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int block) {
+    int block, const NormPrologue& np = NormPrologue{}) {
   extern __shared__ u32x4 lds[];
   u32x4* xl = lds;                                                                // [MT][G][17]
   float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
@@ -521,9 +625,14 @@ __device__ __forceinline__ void flat_block_rpl(
   //    the weight stream wait for an activation round trip.
   //    Index XM = M*G*16 is the end of x's extent: loads past it read zero.
   u32x4 xv[XB];
+  NormLoads<NORM ? XB : 1> nl_;  // the norm prologue's loads (NORM: the row's residual, delta, weight)
+  if constexpr (NORM) {
+    nl_ = norm_issue<XB, NT>(np, 128 * G, t);
+  } else {
 #pragma unroll
-  for (int i = 0; i < XB; ++i)
-    xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
+    for (int i = 0; i < XB; ++i)
+      xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(t + i * NT) * 16, 0, 0);
+  }
   u32x4 wv[RPL][BITS];
   float sv[RPL], zv[RPL];
 #pragma unroll
@@ -531,8 +640,9 @@ __device__ __forceinline__ void flat_block_rpl(
   __builtin_amdgcn_sched_barrier(0);
 
   // 2. Stage activations and per-group sums (first pass from the loads above).
+  if constexpr (NORM) norm_finish<XB, NT>(nl_, np, 128 * G, t, block == 0, xv);
   stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);
-  for (int base = XB * NT; base < XU; base += XB * NT) {
+  for (int base = XB * NT; !NORM && base < XU; base += XB * NT) {
 #pragma unroll
     for (int i = 0; i < XB; ++i)
       xv[i] = __builtin_amdgcn_raw_buffer_load_b128(xr, (uint32_t)(base + t + i * NT) * 16, 0, 0);
@@ -572,18 +682,18 @@ __device__ __forceinline__ void flat_block_rpl(
   }
 }
 
-template <int BITS, int MT, int NT, int RPL, int XB, bool SW>
+template <int BITS, int MT, int NT, int RPL, int XB, bool SW, bool NORM>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int nblocks) {
+    int nblocks, NormPrologue np) {
   // Slots of the XCD-rounded grid past nblocks get rows = 0 in flat_block (no
   // early return: the argument loads then go out as one batch).
   (void)nblocks;
   if constexpr (RPL == 1)
-    flat_block<BITS, MT, NT, 1, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+    flat_block<BITS, MT, NT, 1, XB, SW, NORM>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(), np);
   else
-    flat_block_rpl<BITS, MT, NT, RPL, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+    flat_block_rpl<BITS, MT, NT, RPL, XB, SW, NORM>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(), np);
 }
 
 // Several independent calls in one launch: block b belongs to the last call
@@ -670,8 +780,8 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
       const int nblocks = (int)((N + R - 1) / R);
       const unsigned blocks = xcd_grid(nblocks);
 #define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                     \
-  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
-         ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, \
+         stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks, NormPrologue{})
 #define LAQ_FLAT_NT(MTV, XBV, NTV)                       \
   do {                                                   \
     if (RPL == 2) LAQ_FLAT_K(MTV, XBV, NTV, 2);          \
@@ -754,8 +864,8 @@ hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, cons
   const int nblocks = (int)((N + R - 1) / R);
   const unsigned blocks = xcd_grid(nblocks);
 #define LAQ_SW_K(MTV, XBV, NTV)                                                                                   \
-  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV, true>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
-         qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV, true, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
+         ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks, NormPrologue{})
 #define LAQ_SW_NT(MTV, XBV)                 \
   do {                                      \
     if (NT == 512) LAQ_SW_K(MTV, XBV, 512); \
@@ -772,6 +882,51 @@ hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, cons
 #undef LAQ_SW_XB
 #undef LAQ_SW_NT
 #undef LAQ_SW_K
+  return hipGetLastError();
+}
+
+bool norm_linear_fits(int64_t K) { return K >= 128 && K % 128 == 0 && K <= 8192; }
+
+template <int BITS>
+hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, const uint16_t* scales,
+                              const uint8_t* zeros, uint16_t* y, int64_t N, int64_t K, bool swiglu,
+                              hipStream_t stream, const LaunchEvents& ev) {
+  // The M = 1 flat kernel's configuration (threads, rows per block, rows per
+  // lane as launch_linear chooses them), with blocks of 256 threads up to 32
+  // groups and 512 up to 64, so that two staging units per thread cover the
+  // row: the prologue needs the whole row in registers before its one
+  // reduction.
+  if (!norm_linear_fits(K) || (swiglu && N % 2 != 0)) return hipErrorInvalidValue;
+  const int G = (int)(K / 128);
+  const int NT = G <= 32 ? 256 : 512;
+  auto lds_bytes = [&](int rows) { return (size_t)G * (kGroupStrideU4 * 16 + 4) + (size_t)rows * G * 4; };
+  int R = max(1, min(NT / G, 4096 / G));
+  int RPL = 1;
+  if (swiglu) {
+    R = max(2, R & ~1);
+  } else if ((N + R - 1) / R * (NT / 64) > kResidentWaves) {
+    const int r1 = min(NT / G, 4096 / (G * 2));
+    if (r1 >= 1 && lds_bytes(2 * r1) <= 64 * 1024) {
+      RPL = 2;
+      R = 2 * r1;
+    }
+  }
+  const size_t lds = lds_bytes(R);
+  const int nblocks = (int)((N + R - 1) / R);
+  const dim3 grid(xcd_grid(nblocks));
+#define LAQ_NORM_K(NTV, RPLV, SWV)                                                                                \
+  launch(linear_flat_kernel<BITS, 1, NTV, RPLV, 2, SWV, true>, grid, dim3(NTV), (uint32_t)lds, stream, ev,       \
+         (const uint16_t*)nullptr, qweight, scales, zeros, y, 1, (int)N, G, R, 1.0f / (float)G, nblocks, np)
+  if (NT == 256) {
+    if (swiglu) LAQ_NORM_K(256, 1, true);
+    else if (RPL == 2) LAQ_NORM_K(256, 2, false);
+    else LAQ_NORM_K(256, 1, false);
+  } else {
+    if (swiglu) LAQ_NORM_K(512, 1, true);
+    else if (RPL == 2) LAQ_NORM_K(512, 2, false);
+    else LAQ_NORM_K(512, 1, false);
+  }
+#undef LAQ_NORM_K
   return hipGetLastError();
 }
 
@@ -844,6 +999,10 @@ template hipError_t launch_linear_swiglu<3>(const uint16_t*, const uint32_t*, co
                                             uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_swiglu<4>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
                                             uint16_t*, int, int64_t, int64_t, hipStream_t, const LaunchEvents&);
+template hipError_t launch_linear_norm<3>(const NormPrologue&, const uint32_t*, const uint16_t*, const uint8_t*,
+                                          uint16_t*, int64_t, int64_t, bool, hipStream_t, const LaunchEvents&);
+template hipError_t launch_linear_norm<4>(const NormPrologue&, const uint32_t*, const uint16_t*, const uint8_t*,
+                                          uint16_t*, int64_t, int64_t, bool, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_group<3>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,

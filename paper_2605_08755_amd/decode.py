@@ -1,6 +1,7 @@
 """One batch-1 decode step of a Qwen3-shaped decoder on the library's kernels.
 
-Each layer: residual add + RMSNorm, the fused q|k|v linear, per-head q/k
+Each layer: residual add + RMSNorm, the fused q|k|v linear (the norm inside
+it when the linear offers laq.add_rmsnorm_linear), per-head q/k
 RMSNorm + rotary embedding + KV-cache append, attention over the cache, the
 o linear, residual add + RMSNorm, the fused gate|up linear, SiLU-and-multiply,
 the down linear (whose output the next layer's first norm adds to the
@@ -45,6 +46,14 @@ class DecodeStep:
     fused_attention: the per-head q/k norm, rotary embedding, cache append
     and attention as laq.decode_attention_qkv (two kernels); False: the
     separate laq.qk_norm_rope and laq.decode_attention calls (three).
+
+    A qkv, gate_up or lm_head callable with an attribute norm_linear =
+    g(residual, delta, norm_weight, eps, residual_out, out) computes the norm
+    before it itself (laq.add_rmsnorm_linear: residual_out = residual + delta,
+    out = RMSNorm(residual_out) * norm_weight, then the linear, one kernel);
+    the step then skips that add_rmsnorm call and continues with the residual
+    in residual_out.  The step keeps two residual buffers for this;
+    `residual` is the one holding the current residual stream.
     """
 
     def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None,
@@ -58,7 +67,8 @@ class DecodeStep:
         self.S_max = S_max
         self.cos_sin = rope_table(S_max, shape["rope_theta"], device)
         f16 = dict(dtype=torch.float16, device=device)
-        self.residual = torch.zeros((1, D), dtype=torch.float32, device=device)
+        self._res = [torch.zeros((1, D), dtype=torch.float32, device=device) for _ in range(2)]
+        self._cur = 0
         self.x0 = torch.zeros((1, D), dtype=torch.float32, device=device)  # the token's embedding
         self.h = torch.empty((1, D), **f16)
         self.qkv = torch.empty((1, (Hq + 2 * Hkv) * HEAD_DIM), **f16)
@@ -76,18 +86,33 @@ class DecodeStep:
                   else laq.attention_workspace_bytes(Hq, S_max))
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
 
+    @property
+    def residual(self):
+        """fp32 [1][hidden]: the residual stream as of the last call issued."""
+        return self._res[self._cur]
+
+    def _norm(self, f, delta, weight, out):
+        """Residual add + RMSNorm, then f: fused into f when it offers it."""
+        g = getattr(f, "norm_linear", None)
+        if g is not None:
+            g(self._res[self._cur], delta, weight, self.s["eps"], self._res[1 - self._cur], out)
+            self._cur = 1 - self._cur
+            return
+        laq.add_rmsnorm(self._res[self._cur], delta, weight, self.s["eps"], out=self.h)
+        f(self.h, out)
+
     def run(self, pos):
         """Decode the token at position pos (attends to positions 0..pos).
         Returns the logits when the step has an LM head, else the final
         norm's output."""
         s = self.s
         Hq, Hkv, eps = s["heads"], s["kv_heads"], s["eps"]
-        self.residual.copy_(self.x0)
+        self._cur = 0
+        self._res[0].copy_(self.x0)
         delta = None
         for l, (f_qkv, f_o, f_gu, f_down) in enumerate(self.linears):
             w_in, w_post, qn, kn = self.norms[l]
-            laq.add_rmsnorm(self.residual, delta, w_in, eps, out=self.h)
-            f_qkv(self.h, self.qkv)
+            self._norm(f_qkv, delta, w_in, self.qkv)
             if self.fused_attention:
                 laq.decode_attention_qkv(self.qkv, qn, kn, self.cos_sin, pos, Hq, Hkv, eps, self.k_caches[l],
                                          self.v_caches[l], out=self.attn, workspace=self.workspace)
@@ -97,15 +122,17 @@ class DecodeStep:
                 laq.decode_attention(self.q, self.k_caches[l], self.v_caches[l], pos + 1, out=self.attn,
                                      workspace=self.workspace)
             f_o(self.attn.view(1, Hq * HEAD_DIM), self.o)
-            laq.add_rmsnorm(self.residual, self.o, w_post, eps, out=self.h)
             if getattr(f_gu, "swiglu", False):
-                f_gu(self.h, self.m)
+                self._norm(f_gu, self.o, w_post, self.m)
             else:
-                f_gu(self.h, self.gu)
+                self._norm(f_gu, self.o, w_post, self.gu)
                 laq.silu_mul(self.gu, out=self.m)
             f_down(self.m, self.down)
             delta = self.down
-        laq.add_rmsnorm(self.residual, delta, self.final_norm, eps, out=self.out)
+        if self.lm_head is not None and getattr(self.lm_head, "norm_linear", None) is not None:
+            self._norm(self.lm_head, delta, self.final_norm, self.logits)
+            return self.logits
+        laq.add_rmsnorm(self._res[self._cur], delta, self.final_norm, eps, out=self.out)
         if self.lm_head is None:
             return self.out
         self.lm_head(self.out, self.logits)

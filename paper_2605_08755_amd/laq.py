@@ -30,7 +30,8 @@ EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profil
            "laq_add_rmsnorm_f16", "laq_qk_norm_rope_f16", "laq_decode_attention_workspace_bytes",
            "laq_decode_attention_f16", "laq_silu_mul_f16", "laq_linear_swiglu_w3g128",
            "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128", "laq_decode_attention_qkv_workspace_bytes",
-           "laq_decode_attention_qkv_f16")
+           "laq_decode_attention_qkv_f16", "laq_add_rmsnorm_linear_w3g128", "laq_add_rmsnorm_linear_w4g128",
+           "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128")
 HEAD_DIM = 128
 
 
@@ -78,8 +79,7 @@ def lib():
             f.argtypes = [ctypes.POINTER(LinearCall), ctypes.c_int32, I64, P]
             f.restype = ctypes.c_int32
         for name in ("laq_linear_w3g128", "laq_linear_w4g128", "laq_linear_swiglu_w3g128",
-                     "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128", "laq_decode_attention_qkv_workspace_bytes",
-           "laq_decode_attention_qkv_f16"):
+                     "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, P, P, I64, I64, I64, P]
             f.restype = ctypes.c_int32
@@ -104,6 +104,11 @@ def lib():
         L.laq_decode_attention_qkv_f16.restype = ctypes.c_int32
         L.laq_silu_mul_f16.argtypes = [P, P, I64, I64, P]
         L.laq_silu_mul_f16.restype = ctypes.c_int32
+        for name in ("laq_add_rmsnorm_linear_w3g128", "laq_add_rmsnorm_linear_w4g128",
+                     "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [P, P, P, F32, P, P, P, P, P, I64, I64, P]
+            f.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -304,6 +309,37 @@ def add_rmsnorm(residual, delta, weight, eps, out=None):
     _check(lib().laq_add_rmsnorm_f16(_ptr(residual), _ptr(delta) if delta is not None else None, _ptr(weight),
                                      _ptr(out), M, D, float(eps), _stream(residual.device)))
     return out
+
+
+def add_rmsnorm_linear(residual, delta, norm_weight, eps, qweight, scales, zeros, bits=3, swiglu=False, out=None,
+                       residual_out=None):
+    """One token's residual add + RMSNorm and the linear after it, in one
+    kernel: r = residual + delta (fp32 [1][K]; delta fp16 or None), x =
+    RMSNorm(r) * norm_weight, y = x w_hat^T (fp16 [1][N], or [1][N/2] =
+    silu(gate) * up with swiglu).  r goes to residual_out (a separate fp32
+    [1][K] buffer) when given; x is not materialized."""
+    import torch
+    assert residual.is_cuda and residual.dtype == torch.float32 and residual.is_contiguous()
+    assert residual.dim() == 2 and residual.shape[0] == 1
+    K = residual.shape[1]
+    N = scales.shape[0]
+    assert norm_weight.dtype == torch.float16 and norm_weight.numel() == K and norm_weight.is_contiguous()
+    if delta is not None:
+        assert delta.dtype == torch.float16 and delta.numel() == K and delta.is_contiguous()
+    if residual_out is not None:
+        assert residual_out.dtype == torch.float32 and residual_out.numel() == K and residual_out.is_contiguous()
+    assert qweight.numel() == packed_words(bits, N, K) and qweight.is_contiguous()
+    assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+    assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+    n_out = N // 2 if swiglu else N
+    y = torch.empty((1, n_out), dtype=torch.float16, device=residual.device) if out is None else out
+    fn = {(3, False): lib().laq_add_rmsnorm_linear_w3g128, (4, False): lib().laq_add_rmsnorm_linear_w4g128,
+          (3, True): lib().laq_add_rmsnorm_linear_swiglu_w3g128,
+          (4, True): lib().laq_add_rmsnorm_linear_swiglu_w4g128}[(bits, bool(swiglu))]
+    _check(fn(_ptr(residual), _ptr(delta) if delta is not None else None, _ptr(norm_weight), float(eps),
+              _ptr(residual_out) if residual_out is not None else None, _ptr(qweight), _ptr(scales), _ptr(zeros),
+              _ptr(y), N, K, _stream(residual.device)))
+    return y
 
 
 def qk_norm_rope(qkv, q_norm_weight, k_norm_weight, cos_sin, pos, Hq, Hkv, eps, k_cache, v_cache, q_out=None):

@@ -112,6 +112,36 @@ def test_linear_swiglu_validation(L, bits):
     assert b"laq_linear_swiglu" in L.laq_last_error()
 
 
+def _nl(L, bits, swiglu=False, r=FAKE, d=FAKE, w=FAKE, eps=1e-6, ro=FAKE + 0x10000, q=FAKE, s=FAKE, z=FAKE,
+        y=FAKE, N=4, K=128):
+    f = {(3, False): L.laq_add_rmsnorm_linear_w3g128, (4, False): L.laq_add_rmsnorm_linear_w4g128,
+         (3, True): L.laq_add_rmsnorm_linear_swiglu_w3g128, (4, True): L.laq_add_rmsnorm_linear_swiglu_w4g128}[
+        (bits, swiglu)]
+    return f(ctypes.c_void_p(r), ctypes.c_void_p(d), ctypes.c_void_p(w), ctypes.c_float(eps), ctypes.c_void_p(ro),
+             ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z), ctypes.c_void_p(y), N, K, None)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("swiglu", [False, True])
+def test_add_rmsnorm_linear_validation(L, bits, swiglu):
+    for kw in ("r", "w", "q", "s", "z", "y"):
+        assert _nl(L, bits, swiglu, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _nl(L, bits, swiglu, N=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _nl(L, bits, swiglu, K=127) == laq.LAQ_ERR_BAD_SHAPE
+    assert _nl(L, bits, swiglu, K=8192 + 128) == laq.LAQ_ERR_BAD_SHAPE   # the row must fit one staging pass
+    assert _nl(L, bits, swiglu, eps=-1.0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _nl(L, bits, swiglu, eps=float("inf")) == laq.LAQ_ERR_BAD_SHAPE
+    assert _nl(L, bits, swiglu, ro=FAKE) == laq.LAQ_ERR_BAD_SHAPE         # residual_out == residual
+    assert _nl(L, bits, swiglu, ro=FAKE + 4 * 128 - 16) == laq.LAQ_ERR_BAD_SHAPE  # overlapping
+    if swiglu:
+        assert _nl(L, bits, swiglu, N=3) == laq.LAQ_ERR_BAD_SHAPE
+    for kw in ("r", "d", "w", "ro", "q"):
+        assert _nl(L, bits, swiglu, **{kw: (FAKE + 0x20000 if kw == "ro" else FAKE) + 8}) == laq.LAQ_ERR_MISALIGNED
+    assert _nl(L, bits, swiglu, s=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert _nl(L, bits, swiglu, y=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_add_rmsnorm_linear" in L.laq_last_error()
+
+
 @pytest.mark.parametrize("bits", [3, 4])
 def test_linear_validation(L, bits):
     for kw in ("x", "q", "s", "z", "y"):

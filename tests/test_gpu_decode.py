@@ -163,6 +163,48 @@ def test_linear_swiglu(M, I, K, bits):
     assert r["ok"], r
 
 
+NORM_LINEAR_CASES = [(3, False, 6144, 2560, True), (4, False, 6144, 2560, True), (3, False, 4100, 4096, True),
+                     (3, False, 300, 8192, True), (3, False, 25000, 2560, True), (3, False, 1031, 2560, False),
+                     (3, True, 2 * 9728, 2560, True), (4, True, 2 * 37, 1024, True), (3, True, 2 * 150, 8192, False)]
+
+
+@pytest.mark.parametrize("bits,swiglu,N,K,with_delta", NORM_LINEAR_CASES)
+def test_add_rmsnorm_linear(bits, swiglu, N, K, with_delta):
+    """laq_add_rmsnorm_linear (residual add + RMSNorm computed by every block
+    of the linear while it stages the row, then the linear; with swiglu the
+    SiLU-and-multiply output stage) against the oracle: the new residual
+    bitwise equal to residual + delta in fp32, the output against the
+    oracle's linear (fp64) on the oracle's RMSNorm rounded to fp16, within the
+    linear tolerance.  Rows of 20, 32 and 64 groups (256- and 512-thread
+    blocks), 25000 rows (two rows per lane), ragged N, no delta; the inputs
+    are left untouched."""
+    say("add_rmsnorm_linear", bits, swiglu, N, K, with_delta)
+    rng = np.random.default_rng(N + K + bits)
+    res = (rng.standard_normal((1, K)) * 3).astype(np.float32)
+    delta = f16(rng, (1, K)) if with_delta else None
+    w = (1 + 0.1 * rng.standard_normal(K)).astype(np.float16)
+    wt = inputs.weights(N, K, cfg=44, layer=bits, proj=N % 97)
+    codes, sc, z = oracle.quantize(wt, bits)
+    rd, dd, wd = dev(res), (dev(delta) if with_delta else None), dev(w)
+    ro = torch.full((1, K), float("nan"), dtype=torch.float32, device=DEV)
+    y = laq.add_rmsnorm_linear(rd, dd, wd, EPS, dev(oracle.pack(codes, bits).view(np.int32)),
+                               dev(sc.view(np.float16)), dev(z), bits, swiglu=swiglu, residual_out=ro)
+    torch.cuda.synchronize()
+    r_exp = res + (delta.astype(np.float32) if with_delta else np.float32(0))
+    assert np.array_equal(ro.cpu().numpy(), r_exp)
+    assert np.array_equal(rd.cpu().numpy(), res) and np.array_equal(wd.cpu().numpy(), w)
+    _, x_ref = OD.add_rmsnorm(res, delta, w, EPS)
+    full = np.asarray(oracle.linear(np.asarray(x_ref).astype(np.float16), codes, sc, z), dtype=np.float64)
+    ref = OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), N // 2) if swiglu else full
+    r = linear_check(y.cpu().numpy(), ref)
+    assert r["ok"], r
+    # deterministic, and without residual_out
+    y2 = laq.add_rmsnorm_linear(rd, dd, wd, EPS, dev(oracle.pack(codes, bits).view(np.int32)),
+                                dev(sc.view(np.float16)), dev(z), bits, swiglu=swiglu)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
 def test_decoder_layer_4b():
     """One Qwen3-4B-shaped decoder layer at position pos = 300 with a filled
     cache: W3 linears and the decode operations on the GPU, against the oracle's
@@ -379,3 +421,116 @@ def test_decode_step_vs_oracle(fused, fused_attention):
         torch.cuda.synchronize()
         assert torch.equal(gstep.logits.view(torch.int16), logits.view(torch.int16))
     del graph
+
+
+def test_decode_step_fused_norms_vs_oracle():
+    """DecodeStep with the norms before q|k|v, before gate|up and before the
+    LM head inside those linears (laq.add_rmsnorm_linear; gate|up with the
+    SiLU output stage) over two Qwen3-4B-shaped layers plus an LM head (4096
+    rows), W3 on oracle-quantized codes, at position 200 of a filled cache:
+    each fused call's new residual equals its input residual plus its delta
+    (fp32), its output matches the oracle's linear on the oracle's RMSNorm of
+    that residual, and attention, o and down match the oracle on the GPU's own
+    stage inputs, within the linear tolerance; the logits of a HIP-graph
+    capture of the step, replayed three times with eager steps between,
+    equal the eager step's bit for bit."""
+    say("decode step with fused norms vs oracle")
+    from paper_2605_08755_amd import decode
+    shape = dict(decode.QWEN3_4B, layers=2, vocab=4096)
+    D, Hq, Hkv, I, S, V, pos = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256, 4096, 200
+    rng = np.random.default_rng(29)
+    rec = []
+
+    def fused(kind, l, q, s, z, swiglu):
+        def f(x, out):  # the plain linear (unused by the step when norm_linear is present)
+            laq.linear(x, q, s, z, 3, out=out)
+
+        def g(res, delta, w, eps, res_out, out):
+            laq.add_rmsnorm_linear(res, delta, w, eps, q, s, z, 3, swiglu=swiglu, out=out, residual_out=res_out)
+            rec.append({"kind": kind, "layer": l, "res": res.clone(), "delta": None if delta is None else delta.clone(),
+                        "res_out": res_out.clone(), "out": out.clone()})
+        f.norm_linear = g
+        f.swiglu = swiglu
+        return f
+
+    def plain(kind, l, q, s, z):
+        def f(x, out):
+            laq.linear(x, q, s, z, 3, out=out)
+            rec.append({"kind": kind, "layer": l, "x": x.clone(), "out": out.clone()})
+        return f
+
+    host, lins = [], []
+    for l in range(2):
+        hl, fl = {}, []
+        for j, (name, N, K) in enumerate((("qkv", (Hq + 2 * Hkv) * 128, D), ("o", D, Hq * 128),
+                                          ("gu", 2 * I, D), ("down", D, I))):
+            hq, (q, s, z) = _quantized(N, K, 45, l, j, interleave_halves=name == "gu")
+            hl[name] = hq
+            fl.append(fused(name, l, q, s, z, name == "gu") if name in ("qkv", "gu") else plain(name, l, q, s, z))
+        host.append(hl)
+        lins.append(fl)
+    h_lm, (q_lm, s_lm, z_lm) = _quantized(V, D, 45, 9, 0)
+    norms_h = [tuple((1 + 0.1 * rng.standard_normal(n)).astype(np.float16) for n in (D, D, 128, 128))
+               for _ in range(2)]
+    fin_h = (1 + 0.1 * rng.standard_normal(D)).astype(np.float16)
+    kc_h = [f16(rng, (Hkv, S, 128)) for _ in range(2)]
+    vc_h = [f16(rng, (Hkv, S, 128)) for _ in range(2)]
+    x0_h = rng.standard_normal((1, D)).astype(np.float32)
+    norms = [tuple(dev(a) for a in nl) for nl in norms_h]
+    kcs, vcs = [dev(a) for a in kc_h], [dev(a) for a in vc_h]
+    step = decode.DecodeStep(shape, [tuple(f) for f in lins], norms, dev(fin_h), kcs, vcs, DEV,
+                             lm_head=fused("lm", 2, q_lm, s_lm, z_lm, False))
+    step.x0.copy_(dev(x0_h))
+    logits = step.run(pos).clone()
+    torch.cuda.synchronize()
+    g = {(e["kind"], e["layer"]): {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in e.items()}
+         for e in rec}
+    assert len(g) == 9
+
+    def check(name, got, ref):
+        r = linear_check(got, ref)
+        assert r["ok"], (name, r)
+
+    def normed(e, w):
+        r_out = e["res"] + (e["delta"].astype(np.float32) if e["delta"] is not None else np.float32(0))
+        assert np.array_equal(e["res_out"], r_out)
+        return np.asarray(OD.rmsnorm(r_out, w, EPS)).astype(np.float16)
+
+    assert np.array_equal(g[("qkv", 0)]["res"], x0_h) and g[("qkv", 0)]["delta"] is None
+    for l in range(2):
+        w_in, w_post, qn, kn = norms_h[l]
+        e_qkv, e_o, e_gu, e_dn = (g[(k, l)] for k in ("qkv", "o", "gu", "down"))
+        if l > 0:
+            assert np.array_equal(e_qkv["res"], g[("gu", l - 1)]["res_out"])
+            assert np.array_equal(e_qkv["delta"], g[("down", l - 1)]["out"])
+        check(("qkv", l), e_qkv["out"], oracle.linear(normed(e_qkv, w_in), *host[l]["qkv"]))
+        q_ref, k_ref, v_ref = OD.qk_norm_rope(e_qkv["out"], qn, kn, pos, Hq, Hkv, 128, EPS, THETA)
+        kc, vc = kcs[l].cpu().numpy(), vcs[l].cpu().numpy()
+        check(("k cache row", l), kc[:, pos], k_ref)
+        assert np.array_equal(vc[:, pos], v_ref.astype(np.float16))
+        check(("attention", l), e_o["x"].reshape(Hq, 128),
+              OD.decode_attention(q_ref.astype(np.float16), kc[:, :pos + 1], vc[:, :pos + 1]))
+        check(("o", l), e_o["out"], oracle.linear(e_o["x"], *host[l]["o"]))
+        assert np.array_equal(e_gu["res"], e_qkv["res_out"]) and np.array_equal(e_gu["delta"], e_o["out"])
+        full = np.asarray(oracle.linear(normed(e_gu, w_post), *host[l]["gu"]), dtype=np.float64)
+        check(("gate|up + silu", l), e_gu["out"], OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I))
+        assert np.array_equal(e_dn["x"], e_gu["out"])
+        check(("down", l), e_dn["out"], oracle.linear(e_dn["x"], *host[l]["down"]))
+    e_lm = g[("lm", 2)]
+    assert np.array_equal(e_lm["res"], g[("gu", 1)]["res_out"]) and np.array_equal(e_lm["delta"], g[("down", 1)]["out"])
+    check("logits", logits.cpu().numpy(), oracle.linear(normed(e_lm, fin_h), *h_lm))
+    assert np.array_equal(step.residual.cpu().numpy(), e_lm["res_out"])
+
+    # HIP graph of the same step (recording wrappers copy tensors, which the graph captures too)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        step.run(pos)
+    for _ in range(3):
+        step.logits.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(step.logits.view(torch.int16), logits.view(torch.int16))
+        step.run(pos)
+        torch.cuda.synchronize()
+        assert torch.equal(step.logits.view(torch.int16), logits.view(torch.int16))
