@@ -430,14 +430,23 @@ __global__ __launch_bounds__(64 * NW) void attn_combine2_kernel(const float* __r
     a0[j] = pt[2 + lane];
     a1[j] = pt[2 + 64 + lane];
   }
-  float M = -INFINITY;
-  for (int t0 = 0; t0 < T; t0 += 64)
-    M = fmaxf(M, wave_max(t0 + lane < T ? base[(int64_t)(t0 + lane) * (kHeadDim + 2)] : -INFINITY));
-  float den = 0.0f;
-  for (int t0 = 0; t0 < T; t0 += 64) {
-    const int tt = t0 + lane;
-    const float* pt = base + (int64_t)min(tt, T - 1) * (kHeadDim + 2);
-    den += wave_sum(tt < T ? expf(pt[0] - M) * pt[1] : 0.0f);
+  // Statistics: lane t holds tile t's maximum and denominator.  Up to 64
+  // tiles one pass loads both; beyond, a pass per 64 tiles for M, then one
+  // for the denominator.
+  float M = -INFINITY, den = 0.0f;
+  if (T <= 64) {
+    const float* pt = base + (int64_t)min(lane, T - 1) * (kHeadDim + 2);
+    const float ml = pt[0], ll = pt[1];
+    M = wave_max(lane < T ? ml : -INFINITY);
+    den = wave_sum(lane < T ? expf(ml - M) * ll : 0.0f);
+  } else {
+    for (int t0 = 0; t0 < T; t0 += 64)
+      M = fmaxf(M, wave_max(t0 + lane < T ? base[(int64_t)(t0 + lane) * (kHeadDim + 2)] : -INFINITY));
+    for (int t0 = 0; t0 < T; t0 += 64) {
+      const int tt = t0 + lane;
+      const float* pt = base + (int64_t)min(tt, T - 1) * (kHeadDim + 2);
+      den += wave_sum(tt < T ? expf(pt[0] - M) * pt[1] : 0.0f);
+    }
   }
   float n0 = 0.0f, n1 = 0.0f;
   for (int j0 = 0; w + NW * j0 < T; j0 += kB) {
