@@ -682,18 +682,30 @@ __device__ __forceinline__ void flat_block_rpl(
   }
 }
 
-template <int BITS, int MT, int NT, int RPL, int XB, bool SW, bool NORM>
+template <int BITS, int MT, int NT, int RPL, int XB, bool SW>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int nblocks, NormPrologue np) {
+    int nblocks) {
   // Slots of the XCD-rounded grid past nblocks get rows = 0 in flat_block (no
   // early return: the argument loads then go out as one batch).
   (void)nblocks;
   if constexpr (RPL == 1)
-    flat_block<BITS, MT, NT, 1, XB, SW, NORM>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(), np);
+    flat_block<BITS, MT, NT, 1, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
   else
-    flat_block_rpl<BITS, MT, NT, RPL, XB, SW, NORM>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(), np);
+    flat_block_rpl<BITS, MT, NT, RPL, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+}
+
+// The same with the residual add + RMSNorm prologue (M = 1; no activation
+// pointer: the row is formed from np).
+template <int NT, int RPL, bool SW, int BITS>
+__global__ __launch_bounds__(NT) void linear_flat_norm_kernel(
+    const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
+    uint16_t* __restrict__ y, int N, int G, int R, float inv_g, NormPrologue np) {
+  if constexpr (RPL == 1)
+    flat_block<BITS, 1, NT, 1, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(), np);
+  else
+    flat_block_rpl<BITS, 1, NT, RPL, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(), np);
 }
 
 // Several independent calls in one launch: block b belongs to the last call
@@ -780,8 +792,8 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
       const int nblocks = (int)((N + R - 1) / R);
       const unsigned blocks = xcd_grid(nblocks);
 #define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                     \
-  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, \
-         stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks, NormPrologue{})
+  launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
+         ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
 #define LAQ_FLAT_NT(MTV, XBV, NTV)                       \
   do {                                                   \
     if (RPL == 2) LAQ_FLAT_K(MTV, XBV, NTV, 2);          \
@@ -864,8 +876,8 @@ hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, cons
   const int nblocks = (int)((N + R - 1) / R);
   const unsigned blocks = xcd_grid(nblocks);
 #define LAQ_SW_K(MTV, XBV, NTV)                                                                                   \
-  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV, true, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
-         ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks, NormPrologue{})
+  launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV, true>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
+         qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
 #define LAQ_SW_NT(MTV, XBV)                 \
   do {                                      \
     if (NT == 512) LAQ_SW_K(MTV, XBV, 512); \
@@ -915,8 +927,8 @@ hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, c
   const int nblocks = (int)((N + R - 1) / R);
   const dim3 grid(xcd_grid(nblocks));
 #define LAQ_NORM_K(NTV, RPLV, SWV)                                                                                \
-  launch(linear_flat_kernel<BITS, 1, NTV, RPLV, 2, SWV, true>, grid, dim3(NTV), (uint32_t)lds, stream, ev,       \
-         (const uint16_t*)nullptr, qweight, scales, zeros, y, 1, (int)N, G, R, 1.0f / (float)G, nblocks, np)
+  launch(linear_flat_norm_kernel<NTV, RPLV, SWV, BITS>, grid, dim3(NTV), (uint32_t)lds, stream, ev, qweight,      \
+         scales, zeros, y, (int)N, G, R, 1.0f / (float)G, np)
   if (NT == 256) {
     if (swiglu) LAQ_NORM_K(256, 1, true);
     else if (RPL == 2) LAQ_NORM_K(256, 2, false);
