@@ -149,6 +149,33 @@ int main() {
   EXPECT(laq_linear_swiglu_w3g128(P, Q, P, Z, P, 1, 5, 128, nullptr), LAQ_ERR_BAD_SHAPE, "swiglu");
   EXPECT(laq_linear_swiglu_w3g128(P, Q, P, Z, P, 1, 4, 16384 + 128, nullptr), LAQ_ERR_BAD_SHAPE, "swiglu");
   EXPECT(laq_linear_swiglu_w3g128(P, Q, P, Z, P, 3, 4, 4096 + 128, nullptr), LAQ_ERR_BAD_SHAPE, "swiglu");
+
+  // residual add + RMSNorm inside the linear (M = 1)
+  typedef laq_status (*norm_lin_fn)(const float*, const void*, const void*, float, float*, const uint32_t*,
+                                    const void*, const uint8_t*, void*, int64_t, int64_t, void*);
+  const norm_lin_fn nls[] = {laq_add_rmsnorm_linear_w3g128, laq_add_rmsnorm_linear_w4g128,
+                             laq_add_rmsnorm_linear_swiglu_w3g128, laq_add_rmsnorm_linear_swiglu_w4g128};
+  float* const RO = static_cast<float*>(off(1 << 16));
+  for (int i = 0; i < 4; ++i) {
+    const norm_lin_fn f = nls[i];
+    EXPECT(f(nullptr, P, P, 1e-6f, RO, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_NULL_POINTER, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, nullptr, 1e-6f, RO, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_NULL_POINTER, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, 1e-6f, RO, nullptr, P, Z, P, 4, 128, nullptr), LAQ_ERR_NULL_POINTER, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, 1e-6f, RO, Q, P, Z, nullptr, 4, 128, nullptr), LAQ_ERR_NULL_POINTER, "laq_add_rmsnorm_linear");
+    for (const auto& sh : kBadShapes)
+      EXPECT(f(F, P, P, 1e-6f, RO, Q, P, Z, P, sh[0], sh[1], nullptr), LAQ_ERR_BAD_SHAPE, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, 1e-6f, RO, Q, P, Z, P, 4, 8192 + 128, nullptr), LAQ_ERR_BAD_SHAPE, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, -1.0f, RO, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_BAD_SHAPE, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, std::numeric_limits<float>::quiet_NaN(), RO, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_BAD_SHAPE,
+           "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, 1e-6f, F, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_BAD_SHAPE, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, 1e-6f, F + 100, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_BAD_SHAPE, "laq_add_rmsnorm_linear");
+    EXPECT(f(F + 2, P, P, 1e-6f, RO, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_MISALIGNED, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, off(8), P, 1e-6f, RO, Q, P, Z, P, 4, 128, nullptr), LAQ_ERR_MISALIGNED, "laq_add_rmsnorm_linear");
+    EXPECT(f(F, P, P, 1e-6f, RO, Q, off(1), Z, P, 4, 128, nullptr), LAQ_ERR_MISALIGNED, "laq_add_rmsnorm_linear");
+    if (i >= 2)
+      EXPECT(f(F, P, P, 1e-6f, RO, Q, P, Z, P, 5, 128, nullptr), LAQ_ERR_BAD_SHAPE, "laq_add_rmsnorm_linear_swiglu");
+  }
   // the no-allocation linear: split-K partial sums beyond its scratch array
   EXPECT(laq_linear_noalloc_w3g128(P, Q, P, Z, P, 16, 16000, 1LL << 20, nullptr), LAQ_ERR_BAD_SHAPE, "scratch");
   EXPECT(laq_linear_noalloc_w3g128(P, Q, P, Z, P, 16, 16368, 1LL << 24, nullptr), LAQ_ERR_BAD_SHAPE, "scratch");
