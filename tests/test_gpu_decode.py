@@ -165,7 +165,8 @@ def test_linear_swiglu(M, I, K, bits):
 
 NORM_LINEAR_CASES = [(3, False, 6144, 2560, True), (4, False, 6144, 2560, True), (3, False, 4100, 4096, True),
                      (3, False, 300, 8192, True), (3, False, 25000, 2560, True), (3, False, 1031, 2560, False),
-                     (3, True, 2 * 9728, 2560, True), (4, True, 2 * 37, 1024, True), (3, True, 2 * 150, 8192, False)]
+                     (3, True, 2 * 9728, 2560, True), (4, True, 2 * 37, 1024, True), (3, True, 2 * 150, 8192, False),
+                     (3, False, 300, 128, True), (4, False, 517, 1024, False)]
 
 
 @pytest.mark.parametrize("bits,swiglu,N,K,with_delta", NORM_LINEAR_CASES)
@@ -175,9 +176,9 @@ def test_add_rmsnorm_linear(bits, swiglu, N, K, with_delta):
     SiLU-and-multiply output stage) against the oracle: the new residual
     bitwise equal to residual + delta in fp32, the output against the
     oracle's linear (fp64) on the oracle's RMSNorm rounded to fp16, within the
-    linear tolerance.  Rows of 20, 32 and 64 groups (256- and 512-thread
-    blocks), 25000 rows (two rows per lane), ragged N, no delta; the inputs
-    are left untouched."""
+    linear tolerance.  Rows of 1, 8, 20, 32 and 64 groups (256- and
+    512-thread blocks), 25000 rows (two rows per lane), ragged N, no delta;
+    the inputs are left untouched."""
     say("add_rmsnorm_linear", bits, swiglu, N, K, with_delta)
     rng = np.random.default_rng(N + K + bits)
     res = (rng.standard_normal((1, K)) * 3).astype(np.float32)
