@@ -153,13 +153,39 @@ __global__ __launch_bounds__(64) void qk_norm_rope_kernel(const uint16_t* __rest
   dst[i + 64] = f2h(b);
 }
 
+// Weighted value sums of one wave over the P rows of a value tile in LDS
+// (row-major, 128 fp16 per row): lane i accumulates dimensions 2i and 2i + 1
+// (one 32-bit LDS read per row), with row t's weight taken from lane t of pr,
+// over the rows in order.  Rows past the key length must hold finite values
+// (zeros) and weight zero.  Fully unrolled, so the LDS reads of a batch of 8
+// rows are in flight together.
+template <int P>
+__device__ __forceinline__ void value_sums(const u32x4* vt, float pr, int lane, float& o_even, float& o_odd) {
+  const uint32_t* vw = reinterpret_cast<const uint32_t*>(vt);
+  float e = 0.0f, o = 0.0f;
+#pragma unroll
+  for (int t0 = 0; t0 < P; t0 += 8) {
+    uint32_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = vw[(t0 + j) * (kHeadDim / 2) + lane];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pr), t0 + j));
+      e = fmaf(pt, h2f((uint16_t)(v[j] & 0xFFFFu)), e);
+      o = fmaf(pt, h2f((uint16_t)(v[j] >> 16)), o);
+    }
+  }
+  o_even = e;
+  o_odd = o;
+}
+
 // Partial attention of one key/value head over 64 positions: a block of R
 // waves, wave w for query head g*R + w of the group.  The block loads the
 // tile's key and value rows (16 KiB each, contiguous) into LDS with
 // coalesced 16-byte loads, all issued before the first is used; rows past L
 // read zero (buffer extent).  Lane t then scores position 64*tile + t, the
 // wave forms its softmax statistics (max m, sum l of exp(s - m)) and the
-// weighted value sums o (lane i: dimensions i and i + 64), written to
+// weighted value sums o (lane i: dimensions 2i and 2i + 1), written to
 // ws[((h * T) + tile) * 130 + {0: m, 1: l, 2..129: o}].  Key rows sit in LDS
 // with a 16-byte pad (a stride of 17 units), so that lanes reading their own
 // rows spread over the banks.
@@ -179,7 +205,7 @@ __global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int npos = min(kAttnTile, L - tile * kAttnTile);
+  const int npos = __builtin_amdgcn_readfirstlane(min(kAttnTile, L - tile * kAttnTile));
   const int64_t row0 = (int64_t)g * S_max + (int64_t)tile * kAttnTile;
   const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kc + row0 * kHeadDim),
                                                                      (short)0, npos * kHeadDim * 2, 0x00020000);
@@ -193,8 +219,14 @@ __global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __
     va[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, u * 16, 0, 0);
   }
   const float scale = 0.08838834764831845f;  // 1 / sqrt(128)
-  for (int k = tid; k < R * kHeadDim; k += 64 * R)
-    qs[k / kHeadDim][k % kHeadDim] = h2f(q[((int64_t)g * R) * kHeadDim + k]) * scale;
+  float qv[2];  // the group's R query heads: R * 128 values, two per thread, both loads in flight
+#pragma unroll
+  for (int i = 0; i < 2; ++i) qv[i] = h2f(q[((int64_t)g * R) * kHeadDim + tid + i * 64 * R]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int k = tid + i * 64 * R;
+    qs[k / kHeadDim][k % kHeadDim] = qv[i] * scale;
+  }
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int u = i * 64 * R + tid;
@@ -218,20 +250,15 @@ __global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __
   const float m = wave_max(sv);
   const float pr = valid ? expf(sv - m) : 0.0f;
   const float l = wave_sum(pr);
-  float o0 = 0.0f, o1 = 0.0f;
-  const uint16_t* vh = reinterpret_cast<const uint16_t*>(vt);
-  for (int t = 0; t < npos; ++t) {
-    const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pr), t));
-    o0 = fmaf(pt, h2f(vh[t * kHeadDim + lane]), o0);
-    o1 = fmaf(pt, h2f(vh[t * kHeadDim + lane + 64]), o1);
-  }
+  // value rows past L were loaded as zeros (buffer extent) and weigh zero
+  float oe, oo;
+  value_sums<kAttnTile>(vt, pr, lane, oe, oo);
   float* wp = ws + ((int64_t)(g * R + w) * T + tile) * (kHeadDim + 2);
   if (lane == 0) {
     wp[0] = m;
     wp[1] = l;
   }
-  wp[2 + lane] = o0;
-  wp[2 + 64 + lane] = o1;
+  *reinterpret_cast<float2*>(wp + 2 + 2 * lane) = float2{oe, oo};
 }
 
 // Combines the T partials of each query head in tile order: one wave per
@@ -310,7 +337,7 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = pos + 1;
   const int p0 = tile * P;
-  const int nload = max(0, min(P, pos - p0));  // cache rows read from memory
+  const int nload = __builtin_amdgcn_readfirstlane(max(0, min(P, pos - p0)));  // cache rows read from memory
   const int64_t row0 = (int64_t)g * S_max + p0;
   const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kc + row0 * kHeadDim),
                                                                      (short)0, nload * kHeadDim * 2, 0x00020000);
@@ -341,10 +368,13 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
   const float scale = 0.08838834764831845f;  // 1 / sqrt(128)
   qs[w][lane] = h2f(f2h(a)) * scale;
   qs[w][lane + 64] = h2f(f2h(b)) * scale;
+  // Rows past nload were read as zeros (buffer extent); every row but the new
+  // token's (written below) is staged, so the tile holds finite values only.
+  const int own_row = own ? pos - p0 : -1;
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int u = i * kThreads + tid;
-    if (u < kUnits && (u >> 4) < nload) {
+    if (u < kUnits && (u >> 4) != own_row) {
       kt[(u >> 4) * kKeyStrideU4 + (u & 15)] = ka[i];
       vt[u] = va[i];
     }
@@ -387,21 +417,14 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
   const float m = wave_max(sv);
   const float pr = (valid && c == 0) ? expf(sv - m) : 0.0f;
   const float l = wave_sum(pr);
-  float o0 = 0.0f, o1 = 0.0f;
-  const uint16_t* vh = reinterpret_cast<const uint16_t*>(vt);
-  const int npos = min(P, L - p0);
-  for (int tt = 0; tt < npos; ++tt) {
-    const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pr), tt));
-    o0 = fmaf(pt, h2f(vh[tt * kHeadDim + lane]), o0);
-    o1 = fmaf(pt, h2f(vh[tt * kHeadDim + lane + 64]), o1);
-  }
+  float oe, oo;
+  value_sums<P>(vt, pr, lane, oe, oo);
   float* wp = ws + ((int64_t)(g * R + w) * T + tile) * (kHeadDim + 2);
   if (lane == 0) {
     wp[0] = m;
     wp[1] = l;
   }
-  wp[2 + lane] = o0;
-  wp[2 + 64 + lane] = o1;
+  *reinterpret_cast<float2*>(wp + 2 + 2 * lane) = float2{oe, oo};
 }
 
 // Combines the T partials of one query head (block h of NW waves): every wave
