@@ -206,6 +206,35 @@ def time_graph(stack, M, bits, steps, warmup, step_fn=None):
     return ms, wall
 
 
+def replay_distribution(stack, M, bits, reps=100, warmup=10):
+    """Per-replay step times of the captured step: `reps` replays, each
+    bracketed by its own pair of events on the replay stream, after `warmup`
+    replays; median and 10th / 90th percentiles in microseconds.  A separate
+    pass from the headline's timed region (the events between replays add a
+    little to each one)."""
+    import torch
+    stream = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    stack.step(M, bits)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=stream):
+        stack.step(M, bits)
+    with torch.cuda.stream(stream):
+        for _ in range(warmup):
+            g.replay()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record(stream)
+            g.replay()
+            b.record(stream)
+    torch.cuda.synchronize()
+    us = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+    pick = lambda f: us[min(len(us) - 1, int(round(f * (len(us) - 1))))]
+    del g
+    return {"reps": reps, "median_us": round(pick(0.5), 2), "p10_us": round(pick(0.1), 2),
+            "p90_us": round(pick(0.9), 2), "min_us": round(us[0], 2), "max_us": round(us[-1], 2)}
+
+
 def time_calls_graph(fn, reps=5):
     """Capture the launches fn() makes into a HIP graph and time `reps`
     replays on the current stream: ms per pass, with no host launch gaps."""
@@ -734,11 +763,14 @@ def main():
 
     per_call = per_call_graph(stack, 1, 3)
     log("per call shape (graph of each shape's calls):", per_call)
+    dist = replay_distribution(stack, 1, 3)
+    log("per-replay step times (W3, M=1):", dist)
     extra = {"us_per_step_graph": round(ms * 1e3, 2), "unfused": unfused, "pct_of_hbm_peak": round(value / HBM_PEAK_GBS * 100, 2),
              "launches_per_step": n_launch, "per_call_graph": per_call,
              "eager_kernel_events": {"sum_us_per_step": round(ksum_ms * 1e3, 2),
                                      "avg_us": round(ksum_ms * 1e3 / n_launch, 3)},
              "per_projection": per_proj,
+             "step_us_distribution": dist,
              "wall_s_timed_region": round(wall, 4)}
 
     if not args.no_sweep:
