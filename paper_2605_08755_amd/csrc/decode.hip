@@ -155,14 +155,15 @@ __global__ __launch_bounds__(64) void qk_norm_rope_kernel(const uint16_t* __rest
 
 // Weighted value sums of one wave over the P rows of a value tile in LDS
 // (row-major, 128 fp16 per row): lane i accumulates dimensions 2i and 2i + 1
-// (one 32-bit LDS read per row), with row t's weight taken from lane t of pr,
-// over the rows in order.  Rows past the key length must hold finite values
-// (zeros) and weight zero.  Fully unrolled, so the LDS reads of a batch of 8
-// rows are in flight together.
+// (one 32-bit LDS read per row), with row t's weight taken from lane t of pr.
+// Row t goes to accumulator t % 4 (rows in order within each), and the four
+// are added as (a0 + a1) + (a2 + a3): four independent chains instead of one.
+// Rows past the key length must hold finite values (zeros) and weight zero.
+// Fully unrolled, so the LDS reads of a batch of 8 rows are in flight together.
 template <int P>
 __device__ __forceinline__ void value_sums(const u32x4* vt, float pr, int lane, float& o_even, float& o_odd) {
   const uint32_t* vw = reinterpret_cast<const uint32_t*>(vt);
-  float e = 0.0f, o = 0.0f;
+  float e[4] = {0.0f, 0.0f, 0.0f, 0.0f}, o[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int t0 = 0; t0 < P; t0 += 8) {
     uint32_t v[8];
@@ -171,12 +172,12 @@ __device__ __forceinline__ void value_sums(const u32x4* vt, float pr, int lane, 
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float pt = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pr), t0 + j));
-      e = fmaf(pt, h2f((uint16_t)(v[j] & 0xFFFFu)), e);
-      o = fmaf(pt, h2f((uint16_t)(v[j] >> 16)), o);
+      e[j & 3] = fmaf(pt, h2f((uint16_t)(v[j] & 0xFFFFu)), e[j & 3]);
+      o[j & 3] = fmaf(pt, h2f((uint16_t)(v[j] >> 16)), o[j & 3]);
     }
   }
-  o_even = e;
-  o_odd = o;
+  o_even = (e[0] + e[1]) + (e[2] + e[3]);
+  o_odd = (o[0] + o[1]) + (o[2] + o[3]);
 }
 
 // Partial attention of one key/value head over 64 positions: a block of R
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __
                                                               const uint16_t* __restrict__ kc,
                                                               const uint16_t* __restrict__ vc, int64_t S_max,
                                                               int L, int T, float* __restrict__ ws) {
-  __shared__ float qs[R][kHeadDim];
+  __shared__ u32x4 qh[R][kHeadDim / 8];  // the group's query heads, fp16, 8 per unit
   __shared__ u32x4 kt[kAttnTile * kKeyStrideU4];
   __shared__ u32x4 vt[kAttnTile * kHeadDim / 8];
   constexpr int kUnits = kAttnTile * kHeadDim / 8;  // 16-byte units per tile
@@ -218,15 +219,12 @@ __global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __
     ka[i] = __builtin_amdgcn_raw_buffer_load_b128(kr, u * 16, 0, 0);
     va[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, u * 16, 0, 0);
   }
-  const float scale = 0.08838834764831845f;  // 1 / sqrt(128)
-  float qv[2];  // the group's R query heads: R * 128 values, two per thread, both loads in flight
+  uint16_t qv[2];  // the group's R query heads: R * 128 values, two per thread, both loads in flight
 #pragma unroll
-  for (int i = 0; i < 2; ++i) qv[i] = h2f(q[((int64_t)g * R) * kHeadDim + tid + i * 64 * R]);
+  for (int i = 0; i < 2; ++i) qv[i] = q[((int64_t)g * R) * kHeadDim + tid + i * 64 * R];
+  uint16_t* qh16 = reinterpret_cast<uint16_t*>(&qh[0][0]);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int k = tid + i * 64 * R;
-    qs[k / kHeadDim][k % kHeadDim] = qv[i] * scale;
-  }
+  for (int i = 0; i < 2; ++i) qh16[tid + i * 64 * R] = qv[i];
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int u = i * 64 * R + tid;
@@ -235,17 +233,22 @@ __global__ __launch_bounds__(64 * R) void attn_partial_kernel(const uint16_t* __
   }
   __syncthreads();
 
+  // score of position p: key and query pairs through v_dot2_f32_f16 into four
+  // accumulators (pair j of a unit to accumulator j), (a0 + a1) + (a2 + a3),
+  // scaled by 1/sqrt(128)
   const int p = tile * kAttnTile + lane;
   const bool valid = p < L;
-  float sc = 0.0f;
+  float sa[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int c = 0; c < kHeadDim / 8; ++c) {
     const u32x4 kv = kt[lane * kKeyStrideU4 + c];
-    const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      sc = fmaf(h2f((uint16_t)(wv[e >> 1] >> (16 * (e & 1)))), qs[w][c * 8 + e], sc);
+    const u32x4 qu = qh[w][c];
+    sa[0] = __builtin_amdgcn_fdot2(as_half2(kv.x), as_half2(qu.x), sa[0], false);
+    sa[1] = __builtin_amdgcn_fdot2(as_half2(kv.y), as_half2(qu.y), sa[1], false);
+    sa[2] = __builtin_amdgcn_fdot2(as_half2(kv.z), as_half2(qu.z), sa[2], false);
+    sa[3] = __builtin_amdgcn_fdot2(as_half2(kv.w), as_half2(qu.w), sa[3], false);
   }
+  const float sc = ((sa[0] + sa[1]) + (sa[2] + sa[3])) * 0.08838834764831845f;  // 1 / sqrt(128)
   const float sv = valid ? sc : -INFINITY;
   const float m = wave_max(sv);
   const float pr = valid ? expf(sv - m) : 0.0f;
@@ -327,7 +330,7 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
   constexpr int kUnits = P * kHeadDim / 8;     // 16-byte units of keys (and of values) per tile
   constexpr int kThreads = 64 * R;
   constexpr int kPer = (kUnits + kThreads - 1) / kThreads;
-  __shared__ float qs[R][kHeadDim];
+  __shared__ u32x4 qh[R][kHeadDim / 8];  // the wave's query head, fp16, 8 per unit
   __shared__ u32x4 kt[P * kKeyStrideU4];
   __shared__ u32x4 vt[P * kHeadDim / 8];
   const int g = blockIdx.x;
@@ -365,9 +368,9 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
     v1 = vsrc[lane + 64];
   }
   norm_rope_pair(a, b, qw, cs, eps, lane);
-  const float scale = 0.08838834764831845f;  // 1 / sqrt(128)
-  qs[w][lane] = h2f(f2h(a)) * scale;
-  qs[w][lane + 64] = h2f(f2h(b)) * scale;
+  uint16_t* qh16 = reinterpret_cast<uint16_t*>(qh[w]);
+  qh16[lane] = f2h(a);
+  qh16[lane + 64] = f2h(b);
   // Rows past nload were read as zeros (buffer extent); every row but the new
   // token's (written below) is staged, so the tile holds finite values only.
   const int own_row = own ? pos - p0 : -1;
@@ -396,23 +399,31 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
   }
   __syncthreads();
 
-  // scores: lane = (slice c, position t) with t = lane % P, c = lane / P
+  // scores: lane = (slice c, position t) with t = lane % P, c = lane / P; the
+  // slice's key and query pairs through v_dot2_f32_f16 into four accumulators
+  // (pair j of a unit to accumulator j), added as (a0 + a1) + (a2 + a3), then
+  // the slices by a fixed butterfly and the product scaled by 1/sqrt(128).
+  // (Vector elements pass through as_half2 by value: a bit cast applied to an
+  // element expression was compiled as a cast of element 0.)
   const int t = lane % P;
   const int c = lane / P;
   const int p = p0 + t;
   const bool valid = p < L;
-  float sc = 0.0f;
+  float sa[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
   for (int cc = 0; cc < (kHeadDim / 8) / DS; ++cc) {
     const int unit = c * ((kHeadDim / 8) / DS) + cc;
     const u32x4 kv = kt[t * kKeyStrideU4 + unit];
-    const uint32_t wv[4] = {kv.x, kv.y, kv.z, kv.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      sc = fmaf(h2f((uint16_t)(wv[e >> 1] >> (16 * (e & 1)))), qs[w][unit * 8 + e], sc);
+    const u32x4 qv = qh[w][unit];
+    sa[0] = __builtin_amdgcn_fdot2(as_half2(kv.x), as_half2(qv.x), sa[0], false);
+    sa[1] = __builtin_amdgcn_fdot2(as_half2(kv.y), as_half2(qv.y), sa[1], false);
+    sa[2] = __builtin_amdgcn_fdot2(as_half2(kv.z), as_half2(qv.z), sa[2], false);
+    sa[3] = __builtin_amdgcn_fdot2(as_half2(kv.w), as_half2(qv.w), sa[3], false);
   }
+  float sc = (sa[0] + sa[1]) + (sa[2] + sa[3]);
 #pragma unroll
   for (int o = P; o < 64; o <<= 1) sc += __shfl_xor(sc, o, 64);
+  sc *= 0.08838834764831845f;  // 1 / sqrt(128)
   const float sv = valid && c == 0 ? sc : -INFINITY;
   const float m = wave_max(sv);
   const float pr = (valid && c == 0) ? expf(sv - m) : 0.0f;
