@@ -372,6 +372,37 @@ def decode_step_extra(stack, dev, steps, context=1024):
     swiglu_w.clear()
     for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fused_norms", "w3_fused_swiglu_fp16_head"):
         out[name + "_speedup_vs_fp16"] = round(out["fp16"]["us"] / out[name]["us"], 3)
+
+    # Attention alone: a HIP graph of the 36 layers' attention calls (each
+    # layer's own cache, the token at position context - 1), back to back as in
+    # the step, µs per call and the cache bytes read per second.
+    Hq, hd = shape["heads"], 128
+    qkv = torch.randn(((Hq + 2 * Hkv) * hd,), generator=g, device=dev).to(torch.float16)
+    cs = decode.rope_table(context, shape["rope_theta"], dev)
+    att = torch.empty((Hq, hd), dtype=torch.float16, device=dev)
+    q_sep = torch.empty((Hq, hd), dtype=torch.float16, device=dev)
+    ws_f = torch.empty(laq.attention_qkv_workspace_bytes(Hq, Hkv, context), dtype=torch.uint8, device=dev)
+    ws_s = torch.empty(laq.attention_workspace_bytes(Hq, context), dtype=torch.uint8, device=dev)
+    pos = context - 1
+    cache_bytes = 2 * Hkv * context * hd * 2
+
+    def fused():
+        for l in range(shape["layers"]):
+            qn, kn = norms[l][2], norms[l][3]
+            laq.decode_attention_qkv(qkv, qn, kn, cs, pos, Hq, Hkv, 1e-6, caches[l][0], caches[l][1], out=att,
+                                     workspace=ws_f)
+
+    def separate():
+        for l in range(shape["layers"]):
+            qn, kn = norms[l][2], norms[l][3]
+            laq.qk_norm_rope(qkv, qn, kn, cs, pos, Hq, Hkv, 1e-6, caches[l][0], caches[l][1], q_out=q_sep)
+            laq.decode_attention(q_sep, caches[l][0], caches[l][1], pos + 1, out=att, workspace=ws_s)
+
+    att_out = {}
+    for name, fn in (("fused", fused), ("separate", separate)):
+        us = time_calls_graph(fn, reps=20) * 1e3 / shape["layers"]
+        att_out[name] = {"us_per_layer": round(us, 3), "cache_TBps": round(cache_bytes / (us * 1e-6) / 1e12, 3)}
+    out["attention_graph"] = att_out
     return out
 
 
