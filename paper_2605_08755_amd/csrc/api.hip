@@ -134,7 +134,7 @@ laq_status linear_group(const char* fn, const laq_linear_call* calls, int32_t co
     if (!aligned(c.scales, 2) || !aligned(c.y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
     blocks += c.N;  // an upper bound of the grid: at least one row per block
     lc[i] = laq::LinearCall{static_cast<const uint16_t*>(c.x), c.qweight, static_cast<const uint16_t*>(c.scales),
-                            c.zeros, static_cast<uint16_t*>(c.y), (int)c.N, (int)(c.K / 128), 0, 0};
+                            c.zeros, static_cast<uint16_t*>(c.y), (int)c.N, (int)(c.K / 128), 0, 0, 0.0f};
   }
   if (blocks >= (1LL << 31)) return fail(LAQ_ERR_BAD_SHAPE, fn, "the calls' rows must total < 2^31");
   return hip_status(fn, laq::launch_linear_group<BITS>(lc, count, (int)M, static_cast<hipStream_t>(stream), ev));
