@@ -15,13 +15,15 @@
 // 2^(10-p) + q exactly; one packed fp16 add of -(2^(10-p) + z) leaves q - z
 // exactly.  One v_and_or_b32 + one v_pk_add_f16 per two codes.
 //
-// Kernels: one or two 16-row tiles per block, its waves splitting the row's
-// quads, partial sums added in a fixed order through LDS (fewer than 1024
-// tiles); four tiles per block sharing each activation slab, requesting one
-// quad ahead (many tiles, K <= 2560; also the K ranges of split K, whose fp32
-// partials a second kernel adds in order); four or eight tiles per block
-// walking K one quad at a time, two quads ahead (many tiles, longer rows).
-// Every reduction order is fixed, so results are deterministic.
+// Kernels: one wave per quad of a 16-row tile, every load issued at once
+// (rows of at most ten quads: fewer than 1024 tiles, or M <= 4); the same
+// with three tiles per block sharing the quads' slabs (many tiles, rows of at
+// most five quads, M > 4); one or two 16-row tiles per block, its waves
+// splitting the row's quads (fewer tiles, longer rows); four tiles per block
+// over a K range, one quad ahead (split K, whose fp32 partials a second
+// kernel adds in order); four or eight tiles per block walking K one quad at
+// a time, two quads ahead (many tiles, longer rows).  Every reduction order
+// is fixed, so results are deterministic.
 #include <type_traits>
 #include <utility>
 
@@ -510,9 +512,9 @@ __global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Rows of at most five quads (K <= 2560) with many row tiles, and the K
-// ranges of split K.  A block of four waves owns four 16-row tiles, one per
-// wave, and keeps the activation slabs of all its NQ quads (each slab once
+// The K ranges of split K (rows of many quads, fewer than 1024 tiles).  A
+// block of four waves owns four 16-row tiles, one per wave, over a range of
+// NQ quads, and keeps the activation slabs of all its NQ quads (each slab once
 // per block, x[0..M-1][512q .. 512q+511] into LDS by direct-to-LDS loads, four
 // rows per wave; rows past M read zeros) and the wave's weights of all NQ
 // quads (registers).  Quad q + 1 is requested before quad q is computed, so
@@ -632,15 +634,6 @@ __device__ __forceinline__ void mfma_full_block(
       else y[(int64_t)m * N + row0 + nl] = __builtin_bit_cast(uint16_t, (_Float16)yacc[r]);
     }
   }
-}
-
-template <int BITS, int NQ>
-__global__ __launch_bounds__(64 * kFullTiles) void linear_mfma_full_kernel(
-    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
-  const int block = xcd_block();
-  if (block >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
-  mfma_full_block<BITS, NQ>(x, qw, scales, zeros, y, M, N, G, block, 0, nullptr);
 }
 
 // Split K: logical block b = s * tile_blocks + t takes tile block t over the
@@ -867,6 +860,130 @@ linear_mfma_quad_wave_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Many row tiles, rows of at most five quads, more than four activation rows:
+// one wave per (tile, quad) as in the kernel above, with TPB tiles per block
+// sharing the quads' activation slabs, so that a slab of 8 or 16 rows (8 or
+// 16 KiB per quad) serves TPB waves and two blocks of 3 x 5 waves fit on a
+// compute unit at 64 registers: every wave of the grid is resident and issues
+// all its loads at once.  The waves of tile 0 bring slab q into LDS, one
+// barrier publishes the slabs, every wave then reads its fragments group by
+// group; a second barrier frees the slabs for the waves' partials, a third
+// publishes them, and each tile's quads are added in order.  (Measured on
+// MI355X: Qwen3-4B gate|up, 1216 tiles of 5 quads, M = 16 12.4 -> 11.2 us,
+// M = 8 10.5 -> 10.0 us; at M <= 4 one tile per block stays faster, and two
+// tiles per block left M = 16 at 12.8 us.)
+// ---------------------------------------------------------------------------
+template <int BITS, int MT, int TPB>
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8))) void linear_mfma_quad_share_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  extern __shared__ u32x4 wslab[];  // [nq][MT rows][64 pieces]; afterwards [TPB * nq][4][64] fp32 partials
+  constexpr int WL = BITS + 2;
+  const int b = xcd_block();
+  if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
+  const int K = 128 * G;
+  const int nq = (G + 3) / 4;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int t = __builtin_amdgcn_readfirstlane(w / nq);  // tile of the block
+  const int q = w - t * nq;                              // quad of the row
+  const int nl = lane & 15;
+  const int j = lane >> 4;
+  const int64_t row0 = ((int64_t)b * TPB + t) * 16;
+  const int rows = (int)max((int64_t)0, min((int64_t)16, (int64_t)N - row0));
+  u32x4* const sl = wslab + q * (MT * 64);
+
+  const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
+  const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * 4 * G, (uint32_t)rows * BITS * G * 16);
+  const __amdgpu_buffer_rsrc_t sr = rsrc(scales + row0 * G, (uint32_t)rows * G * 2);
+  const __amdgpu_buffer_rsrc_t zr = rsrc(zeros + row0 * G, (uint32_t)rows * G);
+
+  // 1. Tile 0's waves: the quad's slab (MT direct loads); then every wave its weights.
+  if (t == 0) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const int col = 512 * q + 8 * (lane ^ (m & 7));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void*)(sl + m * 64), 16,
+                                               (uint32_t)(m * K + col) * 2 | (uint32_t)!(m < M && col < K) << 31, 0,
+                                               0, 0);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  const QuadWeights<BITS> qwt = load_quad<BITS, kWeightPolicy>(qr, sr, zr, nl, j, q, G, true);
+  __builtin_amdgcn_sched_barrier(0);
+  wait_vmcnt<WL>();  // tile 0: its slab (issued before the weights) has landed; others: nothing to wait for
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();               // every slab published
+
+  const int arow = nl & (MT - 1);
+  const uint32_t abase = lds_addr(sl + arow * 64);
+  const int swz = arow & 7;
+  uint32_t aoff[4];
+#pragma unroll
+  for (int jj = 0; jj < 4; ++jj) aoff[jj] = abase + 16 * ((4 * j + jj) ^ swz);
+
+  // 2. Quarter transposes, exact (q - z) pairs, four MFMAs per group (each
+  //    group's fragments read just before its MFMAs), scale.
+  wait_vmcnt<0>();
+  __builtin_amdgcn_sched_barrier(0);
+  uint32_t wt[BITS][4];
+#pragma unroll
+  for (int p = 0; p < BITS; ++p) {
+    wt[p][0] = qwt.w[p][0];
+    wt[p][1] = qwt.w[p][1];
+    wt[p][2] = qwt.w[p][2];
+    wt[p][3] = qwt.w[p][3];
+    transpose_quarters(wt[p][0], wt[p][1], wt[p][2], wt[p][3]);
+  }
+  uint32_t szj[4];
+  szj[0] = szj[1] = szj[2] = szj[3] = qwt.s | (qwt.z << 16);
+  transpose_quarters(szj[0], szj[1], szj[2], szj[3]);
+  float4_t yacc = float4_t{0.f, 0.f, 0.f, 0.f};
+  u32x4 af[4][4];
+  static_for<4>([&](auto gc) {
+    constexpr int gi = decltype(gc)::value;
+    static_for<4>([&](auto jc) {
+      constexpr int jj = decltype(jc)::value;
+      af[gi][jj] = lds_read_b128_off<256 * gi>(aoff[jj]);
+    });
+    uint32_t wq[BITS];
+#pragma unroll
+    for (int p = 0; p < BITS; ++p) wq[p] = wt[p][gi];
+    uint32_t pr[16];
+    unpack_chunk_exact<BITS>(wq, szj[gi] >> 16, pr);
+    lds_wait(af[gi]);
+    float4_t c = float4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const half8_t bf = frag(pr[4 * jj + 0], pr[4 * jj + 1], pr[4 * jj + 2], pr[4 * jj + 3]);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, af[gi][jj]), bf, c, 0, 0, 0);
+    }
+    const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(szj[gi] & 0xFFFFu));
+    yacc += s * c;
+  });
+  __syncthreads();  // every wave's fragment reads are done: the slabs are free
+  float* part = reinterpret_cast<float*>(wslab) + w * 256;  // [4][64]
+#pragma unroll
+  for (int r = 0; r < 4; ++r) part[r * 64 + lane] = yacc[r];
+  __syncthreads();
+
+  // 3. Outputs of each tile: its nq waves' partials in quad order.
+  const float* red = reinterpret_cast<const float*>(wslab);
+  for (int idx = threadIdx.x; idx < 256 * TPB; idx += blockDim.x) {
+    const int tt = idx >> 8;
+    const int r = (idx >> 6) & 3;
+    const int ln = idx & 63;
+    float v = 0.0f;
+    for (int qq = 0; qq < nq; ++qq) v += red[(tt * nq + qq) * 256 + r * 64 + ln];
+    const int m = 4 * (ln >> 4) + r;
+    const int n = ln & 15;
+    const int64_t r0 = ((int64_t)b * TPB + tt) * 16;
+    if (m < M && r0 + n < N) y[(int64_t)m * N + r0 + n] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+}
+
 }  // namespace
 
 SplitPlan mfma_split_plan(int M, int64_t N, int G) {
@@ -892,10 +1009,24 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   const int G = (int)(K / 128);
   const int nq = (G + 3) / 4;
   const int64_t tiles = (N + 15) / 16;
+  // Many tiles, rows of at most five quads, M > 4: three tiles per block
+  // share the quads' slabs, one wave per (tile, quad).
+  if (tiles >= kMfmaShareMinTiles && nq <= 5 && M > 4) {
+    constexpr int TPB = 3;
+    const int nblocks = (int)((tiles + TPB - 1) / TPB);
+    const dim3 grid(xcd_grid(nblocks)), blk(64 * TPB * nq);
+    if (M > 8)
+      launch(linear_mfma_quad_share_kernel<BITS, 16, TPB>, grid, blk, (uint32_t)nq * 16 * 1024, stream, ev, x,
+             qweight, scales, zeros, y, M, (int)N, G, nblocks);
+    else
+      launch(linear_mfma_quad_share_kernel<BITS, 8, TPB>, grid, blk, (uint32_t)nq * 8 * 1024, stream, ev, x,
+             qweight, scales, zeros, y, M, (int)N, G, nblocks);
+    return hipGetLastError();
+  }
   // Rows of at most kQuadWaveMax quads whose activation slabs fit in LDS: one
   // tile per block, one wave per quad (measured on MI355X against the kernels
-  // below: faster for every Qwen3-4B projection from M = 3, except the
-  // gate|up call, over 1024 tiles, at M > 8).
+  // below: faster for every Qwen3-4B projection from M = 3 that the sharing
+  // kernel above does not take).
   {
     const int MT = M <= 4 ? 4 : M <= 8 ? 8 : 16;
     const size_t lds = (size_t)nq * MT * 1024;
@@ -923,23 +1054,8 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
       return hipGetLastError();
     }
   }
-  // Many tiles: blocks of four tiles share each activation slab through LDS.
-  // Blocks of four tiles fit three to a compute unit (LDS), so up to 768
-  // blocks are resident at once; from 3072 tiles on, blocks of eight (two to a
-  // compute unit).
-  if (tiles >= kMfmaShareMinTiles && nq <= 5) {
-    const int nblocks = (int)((tiles + kFullTiles - 1) / kFullTiles);
-    const dim3 grid(xcd_grid(nblocks)), blk(64 * kFullTiles);
-    const uint32_t lds = (uint32_t)nq * kSlabBytes;
-    switch (nq) {
-      case 1: launch(linear_mfma_full_kernel<BITS, 1>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
-      case 2: launch(linear_mfma_full_kernel<BITS, 2>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
-      case 3: launch(linear_mfma_full_kernel<BITS, 3>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
-      case 4: launch(linear_mfma_full_kernel<BITS, 4>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
-      default: launch(linear_mfma_full_kernel<BITS, 5>, grid, blk, lds, stream, ev, x, qweight, scales, zeros, y, M, (int)N, G, nblocks); break;
-    }
-    return hipGetLastError();
-  }
+  // Many tiles, longer rows: blocks of four or eight tiles walking K share
+  // each activation slab through LDS.
   if (tiles >= kMfmaShareMinTiles) {
     const int tb = tiles >= 3072 ? 8 : 4;
     const int nblocks = (int)((tiles + tb - 1) / tb);

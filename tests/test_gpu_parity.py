@@ -394,6 +394,30 @@ def test_matrix_core_quad_wave(bits, N, K):
         assert r["ok"], (M, r)
 
 
+SHARE_SHAPES = [(16437, 2176), (16400, 128), (19456, 2560), (16389, 1664)]
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+@pytest.mark.parametrize("N,K", SHARE_SHAPES)
+def test_matrix_core_quad_share(bits, N, K):
+    """At least 1024 tiles, rows of at most five quads, M > 4: three tiles per
+    block sharing the quads' activation slabs (8 rows up to M = 8, 16 above).
+    A last block with two real tiles and an idle one, the last tile ragged
+    (N = 16437 = 1027 * 16 + 5, 1028 tiles) and a last quad of one group
+    (K = 2176, 17 groups); a single group (K = 128); the Qwen3-4B gate|up
+    shape; a last block with one real tile (N = 16389: 1025 tiles, ragged) and
+    four quads (K = 1664, 13 groups).  Repeated calls are bit-identical."""
+    say("mfma quad share", bits, N, K)
+    w = inputs.weights(N, K, cfg=23, layer=bits, proj=K % 89)
+    codes, qw, s, z = oracle_packed(w, bits)
+    for M in (5, 8, 9, 16):
+        x = inputs.activations(M, K, cfg=23, layer=M)
+        y = gpu_linear(x, qw, s, z, bits)
+        r = linear_check(y, oracle.linear(x, codes, s, z))
+        assert r["ok"], (M, r)
+        assert np.array_equal(gpu_linear(x, qw, s, z, bits).view(np.uint16), y.view(np.uint16)), M
+
+
 @pytest.mark.parametrize("bits", [3, 4])
 def test_matrix_core_two_tiles_ragged(bits):
     """Rows longer than 10 quads, enough 16-row tiles (>= 256) and long
