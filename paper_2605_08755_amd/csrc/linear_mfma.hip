@@ -1009,9 +1009,10 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   const int G = (int)(K / 128);
   const int nq = (G + 3) / 4;
   const int64_t tiles = (N + 15) / 16;
-  // Many tiles, rows of at most five quads, M > 4: three tiles per block
-  // share the quads' slabs, one wave per (tile, quad).
-  if (tiles >= kMfmaShareMinTiles && nq <= 5 && M > 4) {
+  // Many tiles, rows of at most five quads, M > 4 (W4: M > 8; at M <= 8 the
+  // one-tile blocks below are faster for W4): three tiles per block share
+  // the quads' slabs, one wave per (tile, quad).
+  if (tiles >= kMfmaShareMinTiles && nq <= 5 && M > (BITS == 4 ? 8 : 4)) {
     constexpr int TPB = 3;
     const int nblocks = (int)((tiles + TPB - 1) / TPB);
     const dim3 grid(xcd_grid(nblocks)), blk(64 * TPB * nq);

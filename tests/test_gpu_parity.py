@@ -400,8 +400,9 @@ SHARE_SHAPES = [(16437, 2176), (16400, 128), (19456, 2560), (16389, 1664)]
 @pytest.mark.parametrize("bits", [3, 4])
 @pytest.mark.parametrize("N,K", SHARE_SHAPES)
 def test_matrix_core_quad_share(bits, N, K):
-    """At least 1024 tiles, rows of at most five quads, M > 4: three tiles per
-    block sharing the quads' activation slabs (8 rows up to M = 8, 16 above).
+    """At least 1024 tiles, rows of at most five quads, M > 4 (W4: M > 8, the
+    one-tile blocks below that): three tiles per block sharing the quads'
+    activation slabs (8 rows up to M = 8, 16 above).
     A last block with two real tiles and an idle one, the last tile ragged
     (N = 16437 = 1027 * 16 + 5, 1028 tiles) and a last quad of one group
     (K = 2176, 17 groups); a single group (K = 128); the Qwen3-4B gate|up
