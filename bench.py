@@ -352,6 +352,18 @@ def decode_step_extra(stack, dev, steps, context=1024):
         f = w3_lin(i)
         return with_norm(f, *stack.q[3][i]) if i % 4 == 0 else f
 
+    mlp_ws = laq.mlp_workspace(D, I, dev)  # stream-ordered calls share it
+
+    def w3_merged_mlp_lin(i):
+        # as w3_norm_lin, with norm + gate|up + SiLU + down of the MLP block in
+        # one launch (laq.add_rmsnorm_mlp; the down callable is then unused)
+        f = w3_norm_lin(i)
+        if i % 4 == 2:
+            gu, dn = swiglu_w[i], stack.q[3][i + 1]
+            f.norm_mlp = lambda res, delta, w, eps, res_out, out: laq.add_rmsnorm_mlp(
+                res, delta, w, eps, gu, dn, mlp_ws, out=out, residual_out=res_out)
+        return f
+
     # (the final norm stays a separate call: inside the 151936-row head's
     # 6331 blocks the prologue costs more than the norm's own launch)
     head_w3 = lambda x, out: laq.linear(x, *q_head, 3, out=out)
@@ -359,6 +371,7 @@ def decode_step_extra(stack, dev, steps, context=1024):
     out = {"context": context, "layers": shape["layers"], "vocab": V}
     variants = (("w3", w3_lin, head_w3, True), ("w3_fused_swiglu", w3_swiglu_lin, head_w3, True),
                 ("w3_fused_swiglu_fused_norms", w3_norm_lin, head_w3, True),
+                ("w3_merged_mlp", w3_merged_mlp_lin, head_w3, True),
                 ("w3_fused_swiglu_separate_attention", w3_swiglu_lin, head_w3, False),
                 ("w3_fused_swiglu_fp16_head", w3_swiglu_lin, head_fp16, True), ("fp16", fp16_lin, head_fp16, True))
     for name, mk, head, fused_attention in variants:
@@ -370,7 +383,7 @@ def decode_step_extra(stack, dev, steps, context=1024):
         out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}
         del step
     swiglu_w.clear()
-    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fused_norms", "w3_fused_swiglu_fp16_head"):
+    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fused_norms", "w3_merged_mlp", "w3_fused_swiglu_fp16_head"):
         out[name + "_speedup_vs_fp16"] = round(out["fp16"]["us"] / out[name]["us"], 3)
 
     # Attention alone: a HIP graph of the 36 layers' attention calls (each
@@ -403,6 +416,32 @@ def decode_step_extra(stack, dev, steps, context=1024):
         us = time_calls_graph(fn, reps=20) * 1e3 / shape["layers"]
         att_out[name] = {"us_per_layer": round(us, 3), "cache_TBps": round(cache_bytes / (us * 1e-6) / 1e12, 3)}
     out["attention_graph"] = att_out
+
+    # The MLP block alone: a HIP graph of the 36 layers' MLP blocks (each
+    # layer's own weights), as two launches (norm + gate|up + SiLU, then down)
+    # and as one (laq.add_rmsnorm_mlp), µs per layer.
+    res = [torch.randn((1, D), generator=g, device=dev) for _ in range(2)]
+    o = torch.randn((1, D), generator=g, device=dev).to(torch.float16)
+    m = torch.empty((1, I), dtype=torch.float16, device=dev)
+    y = torch.empty((1, D), dtype=torch.float16, device=dev)
+    gu_w = []
+    for l in range(shape["layers"]):
+        w = stack.fp16[4 * l + 2]
+        gu_w.append(laq.quantize(torch.stack([w[:I], w[I:]], dim=1).reshape(2 * I, -1).contiguous(), 3))
+
+    def two_launch():
+        for l in range(shape["layers"]):
+            laq.add_rmsnorm_linear(res[0], o, norms[l][1], 1e-6, *gu_w[l], 3, swiglu=True, out=m,
+                                   residual_out=res[1])
+            laq.linear(m, *stack.q[3][4 * l + 3], 3, out=y)
+
+    def one_launch():
+        for l in range(shape["layers"]):
+            laq.add_rmsnorm_mlp(res[0], o, norms[l][1], 1e-6, gu_w[l], stack.q[3][4 * l + 3], mlp_ws, out=y,
+                                residual_out=res[1])
+
+    out["mlp_graph"] = {name: {"us_per_layer": round(time_calls_graph(fn, reps=20) * 1e3 / shape["layers"], 3)}
+                        for name, fn in (("two_launch", two_launch), ("merged", one_launch))}
     return out
 
 

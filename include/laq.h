@@ -368,6 +368,47 @@ laq_status laq_add_rmsnorm_linear_swiglu_w4g128(const float *residual, const voi
                                                 const uint8_t *zeros, void *y, int64_t N, int64_t K,
                                                 void *stream);
 
+/* laq_mlp_workspace_bytes -- device workspace (bytes) that
+ * laq_add_rmsnorm_mlp_w3g128 needs for hidden size D and MLP width I
+ * (fp32 partial sums per 128 intermediates, fp32 team sums, counters);
+ * 0 when the shape is not supported. */
+int64_t laq_mlp_workspace_bytes(int64_t D, int64_t I);
+
+/* laq_add_rmsnorm_mlp_w3g128 -- the SwiGLU MLP block of one token in one
+ * launch (the decode step's post-attention half of a decoder layer; Sec. 5,
+ * Table 3 setting; every weight dequantized by Eq. 1 in the App. H format):
+ *   r = residual + delta;  x = fp16(r / sqrt(mean(r^2) + eps) * norm_weight)
+ *   h = fp16(silu(x gate^T) * (x up^T))          (fp16 [I])
+ *   y = fp16(h down^T)                           (fp16 [D])
+ * with the norm as laq_add_rmsnorm_linear_w3g128 and h as
+ * laq_add_rmsnorm_linear_swiglu_w3g128.  The down product is split over I in
+ * slices of 128 (one workgroup each); the slices' fp32 partial sums are added
+ * in a fixed order by the last workgroups to finish, so y is deterministic.
+ *   residual, delta, norm_weight, eps, residual_out  as for
+ *                 laq_add_rmsnorm_linear_w3g128 (K = D).
+ *   gu_qweight, gu_scales, gu_zeros  [in] gate|up weights, 2I rows of D
+ *                 (gate row j, up row j interleaved) as for
+ *                 laq_linear_swiglu_w3g128.
+ *   down_qweight, down_scales, down_zeros  [in] down weights, D rows of I.
+ *   y             [out] fp16 [D].
+ *   workspace     [scratch] device memory, 16-byte aligned, at least
+ *                 laq_mlp_workspace_bytes(D, I) bytes, filled with zeros once
+ *                 before its first use (its counters; each call leaves them
+ *                 zero again); calls in flight need separate workspaces.
+ * Results: y within the linear tolerance of the three-call sequence
+ * laq_add_rmsnorm_linear_swiglu_w3g128 + laq_linear_w3g128 (h can differ by
+ * one fp16 ulp where x does, and the fp32 sums are added in another order);
+ * r bitwise equal to laq_add_rmsnorm_f16's.
+ * Errors: NULL_POINTER; BAD_SHAPE (D or I not a positive multiple of 128,
+ * D > 2560, I > 2^20, eps < 0 or not finite, residual_out overlapping
+ * residual, workspace too small); MISALIGNED. */
+laq_status laq_add_rmsnorm_mlp_w3g128(const float *residual, const void *delta, const void *norm_weight,
+                                      float eps, float *residual_out, const uint32_t *gu_qweight,
+                                      const void *gu_scales, const uint8_t *gu_zeros,
+                                      const uint32_t *down_qweight, const void *down_scales,
+                                      const uint8_t *down_zeros, void *y, int64_t D, int64_t I,
+                                      void *workspace, int64_t workspace_bytes, void *stream);
+
 /* laq_add_rmsnorm_f16 -- residual update and RMSNorm, row by row:
  *   r = residual + delta;  y = fp16(r / sqrt(mean(r^2) + eps) * weight)
  *   residual  [in/out] fp32 [M][D]; receives r (may be read by later calls).

@@ -398,9 +398,60 @@ laq_status norm_linear(const char* fn, const float* residual, const void* delta,
                                                       static_cast<hipStream_t>(stream), ev));
 }
 
+template <int BITS>
+laq_status norm_mlp(const char* fn, const float* residual, const void* delta, const void* norm_weight, float eps,
+                    float* residual_out, const uint32_t* gu_qweight, const void* gu_scales, const uint8_t* gu_zeros,
+                    const uint32_t* down_qweight, const void* down_scales, const uint8_t* down_zeros, void* y,
+                    int64_t D, int64_t I, void* workspace, int64_t workspace_bytes, void* stream) {
+  const laq::LaunchEvents ev = take_events();
+  if (!residual || !norm_weight || !gu_qweight || !gu_scales || !gu_zeros || !down_qweight || !down_scales ||
+      !down_zeros || !y || !workspace)
+    return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  const laq::MlpPlan p = laq::mlp_plan(D, I, BITS);
+  if (p.S == 0)
+    return fail(LAQ_ERR_BAD_SHAPE, fn,
+                "need D and I positive multiples of 128, D <= 2560, I <= 2^20, and the down group's codes in LDS");
+  if (!(eps >= 0.0f) || !(eps < INFINITY)) return fail(LAQ_ERR_BAD_SHAPE, fn, "eps must be finite and >= 0");
+  if (residual_out != nullptr && residual_out < residual + D && residual < residual_out + D)
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "residual_out must not overlap residual");
+  if (workspace_bytes < (int64_t)laq::mlp_workspace_bytes(p, D))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "workspace smaller than laq_mlp_workspace_bytes(D, I)");
+  if (!aligned(residual, 16) || !aligned(delta, 16) || !aligned(norm_weight, 16) || !aligned(residual_out, 16) ||
+      !aligned(gu_qweight, 16) || !aligned(down_qweight, 16) || !aligned(workspace, 16))
+    return fail(LAQ_ERR_MISALIGNED, fn,
+                "residual, residual_out, delta, norm_weight, both qweights and workspace must be 16-byte aligned");
+  if (!aligned(gu_scales, 2) || !aligned(down_scales, 2) || !aligned(y, 2))
+    return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  laq::NormPrologue np;
+  np.res_in = residual;
+  np.delta = static_cast<const uint16_t*>(delta);
+  np.weight = static_cast<const uint16_t*>(norm_weight);
+  np.res_out = residual_out;
+  np.eps = eps;
+  return hip_status(fn, laq::launch_mlp<BITS>(np, gu_qweight, static_cast<const uint16_t*>(gu_scales), gu_zeros,
+                                               down_qweight, static_cast<const uint16_t*>(down_scales), down_zeros,
+                                               static_cast<uint16_t*>(y), D, I, workspace,
+                                               static_cast<hipStream_t>(stream), ev));
+}
+
 }  // namespace
 
 extern "C" {
+
+int64_t laq_mlp_workspace_bytes(int64_t D, int64_t I) {
+  const laq::MlpPlan p = laq::mlp_plan(D, I, 3);
+  return (int64_t)laq::mlp_workspace_bytes(p, D);
+}
+
+laq_status laq_add_rmsnorm_mlp_w3g128(const float* residual, const void* delta, const void* norm_weight, float eps,
+                                      float* residual_out, const uint32_t* gu_qweight, const void* gu_scales,
+                                      const uint8_t* gu_zeros, const uint32_t* down_qweight, const void* down_scales,
+                                      const uint8_t* down_zeros, void* y, int64_t D, int64_t I, void* workspace,
+                                      int64_t workspace_bytes, void* stream) {
+  return norm_mlp<3>("laq_add_rmsnorm_mlp_w3g128", residual, delta, norm_weight, eps, residual_out, gu_qweight,
+                     gu_scales, gu_zeros, down_qweight, down_scales, down_zeros, y, D, I, workspace, workspace_bytes,
+                     stream);
+}
 
 laq_status laq_linear_swiglu_w3g128(const void* x, const uint32_t* qweight, const void* scales,
                                     const uint8_t* zeros, void* y, int64_t M, int64_t N, int64_t K, void* stream) {

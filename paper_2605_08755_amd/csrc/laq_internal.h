@@ -149,6 +149,25 @@ hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, c
                               const uint8_t* zeros, uint16_t* y, int64_t N, int64_t K, bool swiglu,
                               hipStream_t stream, const LaunchEvents& ev);
 
+// The SwiGLU MLP block of one token in one launch (linear.hip): norm
+// prologue, gate|up + SiLU-and-multiply, down split over the intermediate
+// dimension in S slices of 128, partials added by the last-arriving blocks
+// in T teams.  S == 0: the shape is not supported.
+constexpr int64_t kMlpMaxHidden = 2560;      // D: 256 x D/128 gate|up units over 1024 threads, <= 5 each
+constexpr int64_t kMlpMaxInter = 1 << 20;    // I
+constexpr size_t kMlpLdsBytes = 160 * 1024 - 256;  // LDS of one MI355X compute unit, less the static arrays
+struct MlpPlan {
+  int S = 0, T = 0, team_size = 0;
+  size_t lds = 0;
+};
+MlpPlan mlp_plan(int64_t D, int64_t I, int bits);
+// fp32 partials [S][D], team sums [T][D], then T + 1 uint32 counters.
+size_t mlp_workspace_bytes(const MlpPlan& p, int64_t D);
+template <int BITS>
+hipError_t launch_mlp(const NormPrologue& np, const uint32_t* gu_qw, const uint16_t* gu_s, const uint8_t* gu_z,
+                      const uint32_t* dn_qw, const uint16_t* dn_s, const uint8_t* dn_z, uint16_t* y, int64_t D,
+                      int64_t I, void* workspace, hipStream_t stream, const LaunchEvents& ev);
+
 // Decode-step operations (decode.hip); head dimension 128.
 int64_t decode_attention_tiles(int64_t L);
 hipError_t launch_add_rmsnorm(float* res, const uint16_t* delta, const uint16_t* w, uint16_t* y, int64_t M,

@@ -723,6 +723,262 @@ __global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup
   flat_block<BITS, MT, NT, 1, XB>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, c.R, c.inv_g, b - c.first_block);
 }
 
+// ---------------------------------------------------------------------------
+// The SwiGLU MLP block of one token in one launch: residual add + RMSNorm,
+// the gate|up linear with SiLU-and-multiply, and the down linear (the
+// decode step's post-attention half of a decoder layer, Sec. 5 / Table 3
+// setting, with every weight W3G128 or W4G128 under Eq. 1).
+//
+// The down linear is split over the intermediate dimension I: slice b
+// (logical block b) owns intermediates [128b, 128b + 128), which are the
+// 256 interleaved gate|up rows 256b .. 256b + 255 and group b of every down
+// row.  The block
+//   1. loads everything it needs at once: the residual row, the norm weight
+//      and the delta (registers), its gate|up units (registers, UA per
+//      thread), the scales and zero points of its down group (registers)
+//      and the down codes of its group, D * BITS 16-byte pieces, straight
+//      into LDS;
+//   2. forms x = RMSNorm(residual + delta) as the norm-prologue linear does
+//      and stages it with its group sums;
+//   3. computes its 256 x G1 gate|up unit partials, then h = fp16(silu(gate)
+//      * up) of its 128 intermediates (the fused gate|up linear's output
+//      stage and rounding) and their sum;
+//   4. computes its D down partials s * (sum_k q h - z sum_k h) and writes
+//      them to part[b][0..D).
+// The partials are added in a fixed order without any block waiting on
+// another: slices form teams of team_size consecutive slices; the last block
+// of a team to finish (an atomic counter per team) adds its team's partials
+// in slice order into team[k], and the last of those adders adds the team
+// sums in team order and writes y in fp16.  Each adder resets its counter,
+// so the counters are zero whenever no launch is in flight.
+// ---------------------------------------------------------------------------
+constexpr int kMlpThreads = 1024;
+constexpr int kMlpDownUnits = 3;  // down rows per thread: D <= 3 * 1024
+
+struct MlpArgs {
+  NormPrologue np;
+  const uint32_t* gu_qw;
+  const uint16_t* gu_s;
+  const uint8_t* gu_z;
+  const uint32_t* dn_qw;
+  const uint16_t* dn_s;
+  const uint8_t* dn_z;
+  uint16_t* y;
+  float* part;      // [S][D]
+  float* team;      // [T][D]
+  uint32_t* count;  // [T + 1]
+  int D, G1, S, team_size, T;
+  float inv_g1;
+};
+
+// sum_{j < count} p[j * stride], added in order j = 0, 1, ...; the loads of
+// up to kMlpSumBatch terms are issued together (each is a round trip to
+// memory: one at a time they would serialize).
+constexpr int kMlpSumBatch = 16;
+__device__ __forceinline__ float ordered_sum(const float* p, int stride, int count) {
+  float sum = 0.0f;
+  for (int j0 = 0; j0 < count; j0 += kMlpSumBatch) {
+    float v[kMlpSumBatch];
+#pragma unroll
+    for (int j = 0; j < kMlpSumBatch; ++j) v[j] = p[(size_t)min(j0 + j, count - 1) * stride];
+#pragma unroll
+    for (int j = 0; j < kMlpSumBatch; ++j)
+      if (j0 + j < count) sum += v[j];
+  }
+  return sum;
+}
+
+template <int BITS, int UA>
+__global__ __launch_bounds__(kMlpThreads) void mlp_block_kernel(const MlpArgs a) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  extern __shared__ u32x4 lds[];
+  __shared__ int last;
+  const int D = a.D, G1 = a.G1, G2 = a.S;
+  u32x4* dl = lds;                                        // [D * BITS] down codes of group b
+  u32x4* xl = dl + (size_t)D * BITS;                      // [G1][17] x
+  u32x4* hl = xl + (size_t)G1 * kGroupStrideU4;           // [16] h of the slice
+  float* xsum = reinterpret_cast<float*>(hl + 16);        // [G1]
+  float* pa = xsum + G1;                                  // [256 * G1] gate|up unit partials
+  float* hsum = pa + 256 * G1;                            // [1]
+
+  const int b = xcd_block();
+  if (b >= G2) return;  // XCD-rounding slot
+  const int t = threadIdx.x;
+  const int lane = t & 63, wave = t >> 6;
+
+  const __amdgpu_buffer_rsrc_t qa = make_rsrc(a.gu_qw + (size_t)b * 256 * BITS * G1 * 4, 256u * BITS * G1 * 16);
+  const __amdgpu_buffer_rsrc_t sa = make_rsrc(a.gu_s + (size_t)b * 256 * G1, 256u * G1 * 2);
+  const __amdgpu_buffer_rsrc_t za = make_rsrc(a.gu_z + (size_t)b * 256 * G1, 256u * G1);
+  const __amdgpu_buffer_rsrc_t qd = make_rsrc(a.dn_qw, (uint32_t)D * BITS * G2 * 16);
+  const __amdgpu_buffer_rsrc_t sd = make_rsrc(a.dn_s, (uint32_t)D * G2 * 2);
+  const __amdgpu_buffer_rsrc_t zd = make_rsrc(a.dn_z, (uint32_t)D * G2);
+  const int dr = kMlpThreads / G1, dg = kMlpThreads - (kMlpThreads / G1) * G1;
+  const int r0 = (int)(((float)t + 0.5f) * a.inv_g1);  // t / G1, exact for t < 1024 (see flat_block)
+  const int g0 = t - r0 * G1;
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 1. Loads.  Units past the slice's 256 rows and down rows past D read
+  //    zeros (offsets past the extents).
+  NormLoads<1> nl = norm_issue<1, kMlpThreads>(a.np, D, t);
+  u32x4 wa[UA][BITS];
+  float sva[UA], zva[UA];
+  int ga[UA];
+  {
+    int r = r0, g = g0;
+#pragma unroll
+    for (int i = 0; i < UA; ++i) {
+      load_flat_unit<BITS>(qa, sa, za, r, g, G1, wa[i], sva[i], zva[i]);
+      ga[i] = g;
+      g += dg;
+      r += dr;
+      if (g >= G1) { g -= G1; r += 1; }
+    }
+  }
+  float svd[kMlpDownUnits], zvd[kMlpDownUnits];
+#pragma unroll
+  for (int i = 0; i < kMlpDownUnits; ++i) {
+    const uint32_t u = (uint32_t)(t + i * kMlpThreads) * G2 + b;
+    svd[i] = (float)__builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(sd, u * 2, 0, 0));
+    zvd[i] = (float)__builtin_amdgcn_raw_buffer_load_b8(zd, u, 0, 0);
+  }
+  // Down codes: piece k = n * BITS + p (row n, plane p) of group b to
+  // dl[k]; one instruction moves 64 pieces.  D * BITS is a multiple of 64.
+  for (int j = wave; 64 * j < D * BITS; j += kMlpThreads / 64) {
+    const uint32_t k = (uint32_t)(64 * j + lane);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(qd, (lds_void*)(dl + 64 * j), 16, (k * G2 + b) * 16, 0, 0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 2. x = RMSNorm(residual + delta) * weight, staged with its group sums.
+  u32x4 xv[1];
+  norm_finish<1, kMlpThreads>(nl, a.np, D, t, b == 0, xv);
+  stage_x_pass<1, kMlpThreads, 1>(xv, 0, t, G1 * 16, xl, xsum);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's down pieces are in LDS
+  __syncthreads();
+
+  // 3. Gate|up unit partials, then h and its sum.
+#pragma unroll
+  for (int i = 0; i < UA; ++i) {
+    const int u = t + i * kMlpThreads;
+    if (u < 256 * G1) {
+      const int g = ga[i];
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        uint32_t w[BITS];
+#pragma unroll
+        for (int p = 0; p < BITS; ++p) w[p] = wa[i][p][cc];
+        const u32x4* xp4 = xl + g * kGroupStrideU4 + cc * 4;
+        uint32_t xp[16];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const u32x4 q = xp4[v];
+          xp[4 * v + 0] = q.x;
+          xp[4 * v + 1] = q.y;
+          xp[4 * v + 2] = q.z;
+          xp[4 * v + 3] = q.w;
+        }
+        chunk_dot<BITS>(w, xp, acc);
+      }
+      pa[u] = sva[i] * fmaf(-zva[i], xsum[g], classes_to_value<BITS>(acc));
+    }
+  }
+  __syncthreads();
+  {
+    uint16_t* hh = reinterpret_cast<uint16_t*>(hl);
+    const int l = t & 15;
+    for (int pr = t >> 4; pr < 128; pr += kMlpThreads / 16) {
+      float ag = 0.0f, au = 0.0f;
+      for (int g = l; g < G1; g += 16) {
+        ag += pa[(2 * pr) * G1 + g];
+        au += pa[(2 * pr + 1) * G1 + g];
+      }
+      ag = row16_sum(ag);
+      au = row16_sum(au);
+      if (l == 0) hh[pr] = __builtin_bit_cast(uint16_t, (_Float16)(ag / (1.0f + expf(-ag)) * au));
+    }
+  }
+  __syncthreads();
+  if (t < 16) {
+    const u32x4 hv = hl[t];
+    float ps = dot2(hv.x, kOnesPair, 0.0f);
+    ps = dot2(hv.y, kOnesPair, ps);
+    ps = dot2(hv.z, kOnesPair, ps);
+    ps = dot2(hv.w, kOnesPair, ps);
+    ps = row16_sum(ps);
+    if (t == 0) *hsum = ps;
+  }
+  __syncthreads();
+
+  // 4. Down partials of group b.
+  const float hs = *hsum;
+#pragma unroll
+  for (int i = 0; i < kMlpDownUnits; ++i) {
+    const int n = t + i * kMlpThreads;
+    if (n < D) {
+      u32x4 wv[BITS];
+#pragma unroll
+      for (int p = 0; p < BITS; ++p) wv[p] = dl[n * BITS + p];
+      float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) {
+        uint32_t w[BITS];
+#pragma unroll
+        for (int p = 0; p < BITS; ++p) w[p] = wv[p][cc];
+        uint32_t xp[16];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const u32x4 q = hl[cc * 4 + v];
+          xp[4 * v + 0] = q.x;
+          xp[4 * v + 1] = q.y;
+          xp[4 * v + 2] = q.z;
+          xp[4 * v + 3] = q.w;
+        }
+        chunk_dot<BITS>(w, xp, acc);
+      }
+      a.part[(size_t)b * D + n] = svd[i] * fmaf(-zvd[i], hs, classes_to_value<BITS>(acc));
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's partial stores are done
+
+  // 5. Fixed-order sums by the last-arriving blocks.  Every wave waits for
+  //    its own partial stores to complete (the workgroup barrier alone does
+  //    not wait for global stores), so after the barrier they are all in
+  //    this XCD's L2, and thread 0's device-scope release fence writes them
+  //    back before its counter increment; the adder's thread 0 acquires, and
+  //    the next barrier orders the other waves' loads after it.  (One fence
+  //    per block: a device-scope fence writes back and invalidates the L2, and
+  //    one in every wave measured several times slower.)
+  __syncthreads();
+  const int k = b / a.team_size;
+  const int k0 = k * a.team_size;
+  const int kn = min(a.team_size, G2 - k0);
+  if (t == 0) {
+    __threadfence();
+    const bool l = atomicAdd(&a.count[k], 1u) == (uint32_t)(kn - 1);
+    if (l) __threadfence();
+    last = l;
+  }
+  __syncthreads();
+  if (!last) return;
+  for (int n = t; n < D; n += kMlpThreads)
+    a.team[(size_t)k * D + n] = ordered_sum(a.part + (size_t)k0 * D + n, D, kn);
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's team-sum stores are done
+  __syncthreads();
+  if (t == 0) {
+    atomicExch(&a.count[k], 0u);
+    __threadfence();
+    const bool l = atomicAdd(&a.count[a.T], 1u) == (uint32_t)(a.T - 1);
+    if (l) __threadfence();
+    last = l;
+  }
+  __syncthreads();
+  if (!last) return;
+  for (int n = t; n < D; n += kMlpThreads)
+    a.y[n] = __builtin_bit_cast(uint16_t, (_Float16)ordered_sum(a.team + n, D, a.T));
+  if (t == 0) atomicExch(&a.count[a.T], 0u);
+}
+
 int ceil_pow2(int v) {
   int p = 1;
   while (p < v) p <<= 1;
@@ -942,6 +1198,62 @@ hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, c
   return hipGetLastError();
 }
 
+MlpPlan mlp_plan(int64_t D, int64_t I, int bits) {
+  MlpPlan p;
+  if (D < 128 || D % 128 != 0 || D > kMlpMaxHidden || I < 128 || I % 128 != 0 || I > kMlpMaxInter) return p;
+  const int G1 = (int)(D / 128);
+  const size_t lds = ((size_t)D * bits + (size_t)G1 * kGroupStrideU4 + 16) * 16 + ((size_t)G1 * 257 + 1) * 4;
+  if (lds > kMlpLdsBytes) return p;
+  p.S = (int)(I / 128);
+  p.T = 1;
+  while (p.T * p.T < p.S) ++p.T;  // about sqrt(S) teams of about sqrt(S) slices
+  p.team_size = (p.S + p.T - 1) / p.T;
+  p.T = (p.S + p.team_size - 1) / p.team_size;
+  p.lds = lds;
+  return p;
+}
+
+size_t mlp_workspace_bytes(const MlpPlan& p, int64_t D) {
+  if (p.S == 0) return 0;
+  return ((size_t)(p.S + p.T) * (size_t)D * 4 + (size_t)(p.T + 1) * 4 + 15) / 16 * 16;
+}
+
+template <int BITS>
+hipError_t launch_mlp(const NormPrologue& np, const uint32_t* gu_qw, const uint16_t* gu_s, const uint8_t* gu_z,
+                      const uint32_t* dn_qw, const uint16_t* dn_s, const uint8_t* dn_z, uint16_t* y, int64_t D,
+                      int64_t I, void* workspace, hipStream_t stream, const LaunchEvents& ev) {
+  const MlpPlan p = mlp_plan(D, I, BITS);
+  if (p.S == 0) return hipErrorInvalidValue;
+  MlpArgs a;
+  a.np = np;
+  a.gu_qw = gu_qw;
+  a.gu_s = gu_s;
+  a.gu_z = gu_z;
+  a.dn_qw = dn_qw;
+  a.dn_s = dn_s;
+  a.dn_z = dn_z;
+  a.y = y;
+  a.part = static_cast<float*>(workspace);
+  a.team = a.part + (size_t)p.S * D;
+  a.count = reinterpret_cast<uint32_t*>(a.team + (size_t)p.T * D);
+  a.D = (int)D;
+  a.G1 = (int)(D / 128);
+  a.S = p.S;
+  a.team_size = p.team_size;
+  a.T = p.T;
+  a.inv_g1 = 1.0f / (float)a.G1;
+  const int UA = (a.G1 + 3) / 4;  // 256 rows x G1 groups over 1024 threads
+  const dim3 grid(xcd_grid(p.S)), blk(kMlpThreads);
+  switch (UA) {
+    case 1: launch(mlp_block_kernel<BITS, 1>, grid, blk, (uint32_t)p.lds, stream, ev, a); break;
+    case 2: launch(mlp_block_kernel<BITS, 2>, grid, blk, (uint32_t)p.lds, stream, ev, a); break;
+    case 3: launch(mlp_block_kernel<BITS, 3>, grid, blk, (uint32_t)p.lds, stream, ev, a); break;
+    case 4: launch(mlp_block_kernel<BITS, 4>, grid, blk, (uint32_t)p.lds, stream, ev, a); break;
+    default: launch(mlp_block_kernel<BITS, 5>, grid, blk, (uint32_t)p.lds, stream, ev, a); break;
+  }
+  return hipGetLastError();
+}
+
 template <int BITS>
 hipError_t launch_linear_group(LinearCall* calls, int count, int M, hipStream_t stream, const LaunchEvents& ev) {
   int G_max = 1;
@@ -1015,6 +1327,9 @@ template hipError_t launch_linear_norm<3>(const NormPrologue&, const uint32_t*, 
                                           uint16_t*, int64_t, int64_t, bool, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_norm<4>(const NormPrologue&, const uint32_t*, const uint16_t*, const uint8_t*,
                                           uint16_t*, int64_t, int64_t, bool, hipStream_t, const LaunchEvents&);
+template hipError_t launch_mlp<3>(const NormPrologue&, const uint32_t*, const uint16_t*, const uint8_t*,
+                                  const uint32_t*, const uint16_t*, const uint8_t*, uint16_t*, int64_t, int64_t,
+                                  void*, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_group<3>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_group<4>(LinearCall*, int, int, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,

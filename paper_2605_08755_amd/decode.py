@@ -53,7 +53,11 @@ class DecodeStep:
     out = RMSNorm(residual_out) * norm_weight, then the linear, one kernel);
     the step then skips that add_rmsnorm call and continues with the residual
     in residual_out.  The step keeps two residual buffers for this;
-    `residual` is the one holding the current residual stream.
+    `residual` is the one holding the current residual stream.  A gate_up
+    callable with an attribute norm_mlp (same arguments as norm_linear, out
+    receiving the down projection's output, fp16 [1][hidden]) is the whole MLP
+    block after the attention: norm, gate|up, SiLU-and-multiply and down
+    (laq.add_rmsnorm_mlp, one kernel); the step then skips the down call.
     """
 
     def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None,
@@ -122,6 +126,12 @@ class DecodeStep:
                 laq.decode_attention(self.q, self.k_caches[l], self.v_caches[l], pos + 1, out=self.attn,
                                      workspace=self.workspace)
             f_o(self.attn.view(1, Hq * HEAD_DIM), self.o)
+            mlp = getattr(f_gu, "norm_mlp", None)
+            if mlp is not None:
+                mlp(self._res[self._cur], self.o, w_post, eps, self._res[1 - self._cur], self.down)
+                self._cur = 1 - self._cur
+                delta = self.down
+                continue
             if getattr(f_gu, "swiglu", False):
                 self._norm(f_gu, self.o, w_post, self.m)
             else:

@@ -31,7 +31,8 @@ EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profil
            "laq_decode_attention_f16", "laq_silu_mul_f16", "laq_linear_swiglu_w3g128",
            "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128", "laq_decode_attention_qkv_workspace_bytes",
            "laq_decode_attention_qkv_f16", "laq_add_rmsnorm_linear_w3g128", "laq_add_rmsnorm_linear_w4g128",
-           "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128")
+           "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128",
+           "laq_mlp_workspace_bytes", "laq_add_rmsnorm_mlp_w3g128")
 HEAD_DIM = 128
 
 
@@ -105,10 +106,15 @@ def lib():
         L.laq_silu_mul_f16.argtypes = [P, P, I64, I64, P]
         L.laq_silu_mul_f16.restype = ctypes.c_int32
         for name in ("laq_add_rmsnorm_linear_w3g128", "laq_add_rmsnorm_linear_w4g128",
-                     "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128"):
+                     "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128",
+           "laq_mlp_workspace_bytes", "laq_add_rmsnorm_mlp_w3g128"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, F32, P, P, P, P, P, I64, I64, P]
             f.restype = ctypes.c_int32
+        L.laq_mlp_workspace_bytes.argtypes = [I64, I64]
+        L.laq_mlp_workspace_bytes.restype = I64
+        L.laq_add_rmsnorm_mlp_w3g128.argtypes = [P, P, P, F32, P, P, P, P, P, P, P, P, I64, I64, P, I64, P]
+        L.laq_add_rmsnorm_mlp_w3g128.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -339,6 +345,53 @@ def add_rmsnorm_linear(residual, delta, norm_weight, eps, qweight, scales, zeros
     _check(fn(_ptr(residual), _ptr(delta) if delta is not None else None, _ptr(norm_weight), float(eps),
               _ptr(residual_out) if residual_out is not None else None, _ptr(qweight), _ptr(scales), _ptr(zeros),
               _ptr(y), N, K, _stream(residual.device)))
+    return y
+
+
+def mlp_workspace_bytes(D, I):
+    return int(lib().laq_mlp_workspace_bytes(D, I))
+
+
+def mlp_workspace(D, I, device):
+    """A zero-filled workspace for add_rmsnorm_mlp (its counters start at
+    zero; every call leaves them zero)."""
+    import torch
+    n = mlp_workspace_bytes(D, I)
+    if n <= 0:
+        raise LaqError(LAQ_ERR_BAD_SHAPE, "merged MLP block: unsupported shape D=%d I=%d" % (D, I))
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def add_rmsnorm_mlp(residual, delta, norm_weight, eps, gate_up, down, workspace, out=None, residual_out=None):
+    """One token's SwiGLU MLP block in one launch (W3G128): r = residual +
+    delta, x = RMSNorm(r) * norm_weight, h = silu(x gate^T) * (x up^T), y =
+    h down^T (fp16 [1][D]).  gate_up = (qweight, scales, zeros) of the 2I
+    interleaved gate|up rows, down = (qweight, scales, zeros) of the D down
+    rows; workspace from mlp_workspace(D, I)."""
+    import torch
+    assert residual.is_cuda and residual.dtype == torch.float32 and residual.is_contiguous()
+    assert residual.dim() == 2 and residual.shape[0] == 1
+    D = residual.shape[1]
+    gq, gs, gz = gate_up
+    dq, ds, dz = down
+    I = gs.shape[0] // 2
+    assert norm_weight.dtype == torch.float16 and norm_weight.numel() == D and norm_weight.is_contiguous()
+    if delta is not None:
+        assert delta.dtype == torch.float16 and delta.numel() == D and delta.is_contiguous()
+    if residual_out is not None:
+        assert residual_out.dtype == torch.float32 and residual_out.numel() == D and residual_out.is_contiguous()
+    assert gq.numel() == packed_words(3, 2 * I, D) and gq.is_contiguous()
+    assert gs.shape == (2 * I, D // GROUP) and gz.shape == (2 * I, D // GROUP)
+    assert dq.numel() == packed_words(3, D, I) and dq.is_contiguous()
+    assert ds.shape == (D, I // GROUP) and dz.shape == (D, I // GROUP)
+    assert gs.dtype == torch.float16 and ds.dtype == torch.float16
+    assert gz.dtype == torch.uint8 and dz.dtype == torch.uint8
+    y = torch.empty((1, D), dtype=torch.float16, device=residual.device) if out is None else out
+    _check(lib().laq_add_rmsnorm_mlp_w3g128(
+        _ptr(residual), _ptr(delta) if delta is not None else None, _ptr(norm_weight), float(eps),
+        _ptr(residual_out) if residual_out is not None else None, _ptr(gq), _ptr(gs), _ptr(gz), _ptr(dq), _ptr(ds),
+        _ptr(dz), _ptr(y), D, I, _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _stream(residual.device)))
     return y
 
 

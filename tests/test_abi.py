@@ -142,6 +142,37 @@ def test_add_rmsnorm_linear_validation(L, bits, swiglu):
     assert b"laq_add_rmsnorm_linear" in L.laq_last_error()
 
 
+def _mlp(L, r=FAKE, d=FAKE, w=FAKE, eps=1e-6, ro=FAKE + 0x10000, gq=FAKE, gs=FAKE, gz=FAKE, dq=FAKE, ds=FAKE,
+         dz=FAKE, y=FAKE, D=256, I=384, ws=FAKE, ws_bytes=1 << 20):
+    return L.laq_add_rmsnorm_mlp_w3g128(
+        ctypes.c_void_p(r), ctypes.c_void_p(d), ctypes.c_void_p(w), ctypes.c_float(eps), ctypes.c_void_p(ro),
+        ctypes.c_void_p(gq), ctypes.c_void_p(gs), ctypes.c_void_p(gz), ctypes.c_void_p(dq), ctypes.c_void_p(ds),
+        ctypes.c_void_p(dz), ctypes.c_void_p(y), D, I, ctypes.c_void_p(ws), ws_bytes, None)
+
+
+def test_add_rmsnorm_mlp_validation(L):
+    # workspace: fp32 partials [I/128][D] and team sums, then the counters
+    S = 3
+    T = 2  # about sqrt(S) teams
+    assert L.laq_mlp_workspace_bytes(256, 384) == ((S + T) * 256 * 4 + (T + 1) * 4 + 15) // 16 * 16
+    assert L.laq_mlp_workspace_bytes(2560, 9728) > 0
+    assert L.laq_mlp_workspace_bytes(2560 + 128, 9728) == 0   # D past the register budget
+    assert L.laq_mlp_workspace_bytes(256, 100) == 0
+    for kw in ("r", "w", "gq", "gs", "gz", "dq", "ds", "dz", "y", "ws"):
+        assert _mlp(L, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _mlp(L, D=200) == laq.LAQ_ERR_BAD_SHAPE
+    assert _mlp(L, I=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _mlp(L, D=2688) == laq.LAQ_ERR_BAD_SHAPE
+    assert _mlp(L, eps=-1.0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _mlp(L, ro=FAKE) == laq.LAQ_ERR_BAD_SHAPE                   # residual_out == residual
+    assert _mlp(L, ws_bytes=L.laq_mlp_workspace_bytes(256, 384) - 16) == laq.LAQ_ERR_BAD_SHAPE
+    for kw in ("r", "d", "w", "ro", "gq", "dq", "ws"):
+        assert _mlp(L, **{kw: (FAKE + 0x20000 if kw == "ro" else FAKE) + 8}) == laq.LAQ_ERR_MISALIGNED
+    for kw in ("gs", "ds", "y"):
+        assert _mlp(L, **{kw: FAKE + 1}) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_add_rmsnorm_mlp" in L.laq_last_error()
+
+
 @pytest.mark.parametrize("bits", [3, 4])
 def test_linear_validation(L, bits):
     for kw in ("x", "q", "s", "z", "y"):

@@ -206,6 +206,67 @@ def test_add_rmsnorm_linear(bits, swiglu, N, K, with_delta):
     assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
 
 
+MLP_CASES = [(2560, 9728, True), (256, 384, True), (1024, 128, False), (1280, 128 * 77, True), (2560, 1152, False)]
+
+
+@pytest.mark.parametrize("D,I,with_delta", MLP_CASES)
+def test_add_rmsnorm_mlp(D, I, with_delta):
+    """laq_add_rmsnorm_mlp_w3g128 (the SwiGLU MLP block in one launch: the
+    norm prologue, gate|up with SiLU-and-multiply per slice of 128
+    intermediates, the slice's share of down, partials added by the
+    last-arriving workgroups) against the oracle's composition: the new
+    residual bitwise equal to residual + delta, y against the oracle's down
+    linear (fp64) on h = silu(gate) * up from the oracle's gate|up linear on
+    the oracle's RMSNorm (x and h rounded to fp16 where the kernel rounds
+    them), within the linear tolerance.  Qwen3-4B's D = 2560, I = 9728 (76
+    slices in 9 teams), 3 slices (teams of 2 and 1), one slice, 77 slices (a
+    last team of 5), no delta.  Then three more calls on the same workspace
+    (its counters reset by each call) and three replays of a HIP-graph
+    capture give y bit for bit."""
+    say("add_rmsnorm_mlp", D, I, with_delta)
+    rng = np.random.default_rng(D + I)
+    res = (rng.standard_normal((1, D)) * 3).astype(np.float32)
+    delta = f16(rng, (1, D)) if with_delta else None
+    w = (1 + 0.1 * rng.standard_normal(D)).astype(np.float16)
+    hgu, gu = _quantized(2 * I, D, 46, 0, I % 89, interleave_halves=True)
+    hdn, dn = _quantized(D, I, 46, 1, D % 89)
+    rd, dd, wd = dev(res), (dev(delta) if with_delta else None), dev(w)
+    ro = torch.full((1, D), float("nan"), dtype=torch.float32, device=DEV)
+    ws = laq.mlp_workspace(D, I, DEV)
+    y = laq.add_rmsnorm_mlp(rd, dd, wd, EPS, gu, dn, ws, residual_out=ro)
+    torch.cuda.synchronize()
+    r_exp = res + (delta.astype(np.float32) if with_delta else np.float32(0))
+    assert np.array_equal(ro.cpu().numpy(), r_exp)
+    assert np.array_equal(rd.cpu().numpy(), res)
+    _, x_ref = OD.add_rmsnorm(res, delta, w, EPS)
+    full = np.asarray(oracle.linear(np.asarray(x_ref).astype(np.float16), *hgu), dtype=np.float64)
+    h_ref = OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I)
+    y_ref = oracle.linear(np.asarray(h_ref).astype(np.float16), *hdn)
+    r = linear_check(y.cpu().numpy(), y_ref)
+    assert r["ok"], r
+    S = I // 128
+    T = 1
+    while T * T < S:
+        T += 1
+    T = -(-S // -(-S // T))  # teams of ceil(S / T) slices
+    assert not ws[(S + T) * D * 4:].any()  # the counters are zero again
+    for _ in range(3):
+        y2 = laq.add_rmsnorm_mlp(rd, dd, wd, EPS, gu, dn, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+    out = torch.empty_like(y)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        laq.add_rmsnorm_mlp(rd, dd, wd, EPS, gu, dn, ws, out=out)
+    for _ in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), y.view(torch.int16))
+    del graph
+
+
 def test_decoder_layer_4b():
     """One Qwen3-4B-shaped decoder layer at position pos = 300 with a filled
     cache: W3 linears and the decode operations on the GPU, against the oracle's
@@ -424,7 +485,8 @@ def test_decode_step_vs_oracle(fused, fused_attention):
     del graph
 
 
-def test_decode_step_fused_norms_vs_oracle():
+@pytest.mark.parametrize("merged_mlp", [False, True])
+def test_decode_step_fused_norms_vs_oracle(merged_mlp):
     """DecodeStep with the norms before q|k|v, before gate|up and before the
     LM head inside those linears (laq.add_rmsnorm_linear; gate|up with the
     SiLU output stage) over two Qwen3-4B-shaped layers plus an LM head (4096
@@ -434,8 +496,10 @@ def test_decode_step_fused_norms_vs_oracle():
     that residual, and attention, o and down match the oracle on the GPU's own
     stage inputs, within the linear tolerance; the logits of a HIP-graph
     capture of the step, replayed three times with eager steps between,
-    equal the eager step's bit for bit."""
-    say("decode step with fused norms vs oracle")
+    equal the eager step's bit for bit.  merged_mlp: the MLP block (norm,
+    gate|up, SiLU, down) as one laq.add_rmsnorm_mlp call, its output checked
+    against the oracle's down linear on the oracle's h of the oracle's norm."""
+    say("decode step with fused norms vs oracle, merged mlp =", merged_mlp)
     from paper_2605_08755_amd import decode
     shape = dict(decode.QWEN3_4B, layers=2, vocab=4096)
     D, Hq, Hkv, I, S, V, pos = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256, 4096, 200
@@ -454,13 +518,25 @@ def test_decode_step_fused_norms_vs_oracle():
         f.swiglu = swiglu
         return f
 
+    def merged(l, gu, dn):
+        f = fused("gu", l, *gu, True)
+
+        def g(res, delta, w, eps, res_out, out):
+            laq.add_rmsnorm_mlp(res, delta, w, eps, gu, dn, mlp_ws, out=out, residual_out=res_out)
+            rec.append({"kind": "mlp", "layer": l, "res": res.clone(), "delta": delta.clone(),
+                        "res_out": res_out.clone(), "out": out.clone()})
+        f.norm_mlp = g
+        return f
+
+    mlp_ws = laq.mlp_workspace(2560, 9728, DEV)
+
     def plain(kind, l, q, s, z):
         def f(x, out):
             laq.linear(x, q, s, z, 3, out=out)
             rec.append({"kind": kind, "layer": l, "x": x.clone(), "out": out.clone()})
         return f
 
-    host, lins = [], []
+    host, lins, dev_w = [], [], {}
     for l in range(2):
         hl, fl = {}, []
         for j, (name, N, K) in enumerate((("qkv", (Hq + 2 * Hkv) * 128, D), ("o", D, Hq * 128),
@@ -468,6 +544,9 @@ def test_decode_step_fused_norms_vs_oracle():
             hq, (q, s, z) = _quantized(N, K, 45, l, j, interleave_halves=name == "gu")
             hl[name] = hq
             fl.append(fused(name, l, q, s, z, name == "gu") if name in ("qkv", "gu") else plain(name, l, q, s, z))
+            dev_w[(name, l)] = (q, s, z)
+        if merged_mlp:
+            fl[2] = merged(l, dev_w[("gu", l)], dev_w[("down", l)])
         host.append(hl)
         lins.append(fl)
     h_lm, (q_lm, s_lm, z_lm) = _quantized(V, D, 45, 9, 0)
@@ -486,7 +565,13 @@ def test_decode_step_fused_norms_vs_oracle():
     torch.cuda.synchronize()
     g = {(e["kind"], e["layer"]): {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in e.items()}
          for e in rec}
-    assert len(g) == 9
+    assert len(g) == (7 if merged_mlp else 9)
+    if merged_mlp:
+        # the one-launch MLP block stands for the gate|up and down records
+        for l in range(2):
+            e = g.pop(("mlp", l))
+            g[("gu", l)] = {k: e[k] for k in ("res", "delta", "res_out")}
+            g[("down", l)] = {"out": e["out"]}
 
     def check(name, got, ref):
         r = linear_check(got, ref)
@@ -514,7 +599,11 @@ def test_decode_step_fused_norms_vs_oracle():
         check(("o", l), e_o["out"], oracle.linear(e_o["x"], *host[l]["o"]))
         assert np.array_equal(e_gu["res"], e_qkv["res_out"]) and np.array_equal(e_gu["delta"], e_o["out"])
         full = np.asarray(oracle.linear(normed(e_gu, w_post), *host[l]["gu"]), dtype=np.float64)
-        check(("gate|up + silu", l), e_gu["out"], OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I))
+        h_ref = OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I)
+        if merged_mlp:
+            check(("mlp block", l), e_dn["out"], oracle.linear(np.asarray(h_ref).astype(np.float16), *host[l]["down"]))
+            continue
+        check(("gate|up + silu", l), e_gu["out"], h_ref)
         assert np.array_equal(e_dn["x"], e_gu["out"])
         check(("down", l), e_dn["out"], oracle.linear(e_dn["x"], *host[l]["down"]))
     e_lm = g[("lm", 2)]
