@@ -5,6 +5,10 @@
 All HIP sources are compiled by hipcc for gfx950 only.  Packed-fp32 VALU
 instructions are disabled for the device code (-packed-fp32-ops).  The host
 pass warns that it does not know that feature; the warning is harmless.
+Kernel arguments are preloaded into scalar registers (up to 14 dwords, the
+user-SGPR budget left beside the argument-segment pointer), so a wave's
+first memory requests do not wait for a scalar load of its arguments; the
+kernels order their arguments so that these come first.
 """
 import glob
 import os
@@ -19,6 +23,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-kernarg-preload-count=14",
     "-Wall", "-Wno-unused-command-line-argument",
 ]
 

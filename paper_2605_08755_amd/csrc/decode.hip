@@ -320,11 +320,13 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
 //    the 128 dimensions, added by a fixed butterfly), forms the softmax
 //    statistics and the weighted value sums as attn_partial_kernel does.
 // Partials go to ws[((h * T) + tile) * 130 + {0: m, 1: l, 2..129: o}].
+// Argument order: what the tile's loads and the query's norm need first
+// (the first fourteen dwords arrive preloaded in scalar registers).
 template <int R, int P>
 __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
-    const uint16_t* __restrict__ qkv, const uint16_t* __restrict__ qw, const uint16_t* __restrict__ kw,
-    const float* __restrict__ cs, float eps, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int64_t S_max,
-    int pos, int Hq, int Hkv, int T, float* __restrict__ ws) {
+    uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int S_max, int pos, const uint16_t* __restrict__ qkv,
+    const uint16_t* __restrict__ qw, const float* __restrict__ cs, float eps, int Hq, int Hkv,
+    const uint16_t* __restrict__ kw, int T, float* __restrict__ ws) {
   static_assert(P == 16 || P == 32 || P == 64, "tile of 16, 32 or 64 positions");
   constexpr int DS = 64 / P;                   // lanes per position (dimension slices)
   constexpr int kUnits = P * kHeadDim / 8;     // 16-byte units of keys (and of values) per tile
@@ -594,8 +596,8 @@ hipError_t launch_decode_attention_qkv(const uint16_t* qkv, const uint16_t* qw, 
   const dim3 grid((unsigned)Hkv, (unsigned)T);
   const float* cs = cos_sin + pos * kHeadDim;
 #define LAQ_ATTN_QKV(RV, PV)                                                                                 \
-  launch(attn_qkv_partial_kernel<RV, PV>, grid, dim3(64 * RV), 0, stream, e1, qkv, qw, kw, cs, eps, kc, vc, \
-         S_max, (int)pos, (int)Hq, (int)Hkv, T, ws)
+  launch(attn_qkv_partial_kernel<RV, PV>, grid, dim3(64 * RV), 0, stream, e1, kc, vc, (int)S_max, (int)pos, qkv, \
+         qw, cs, eps, (int)Hq, (int)Hkv, kw, T, ws)
 #define LAQ_ATTN_QKV_P(RV)                 \
   do {                                     \
     if (P == 64) LAQ_ATTN_QKV(RV, 64);     \

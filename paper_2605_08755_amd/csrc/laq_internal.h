@@ -19,14 +19,19 @@ __device__ __forceinline__ half2_t as_half2(uint32_t v) { return __builtin_bit_c
 // XCD-aware block order.  MI355X deals consecutive workgroups of a launch to
 // its eight XCDs in turn, and each XCD has its own L2.  A grid of
 // xcd_grid(nblocks) workgroups (a multiple of 8) whose workgroup b takes
-// logical block xcd_block() = (b % 8) * (grid / 8) + b / 8 gives every XCD a
-// contiguous range of logical blocks (rows); logical blocks >= nblocks are
-// idle and return at once.  Any mapping of workgroups to XCDs gives the same
-// results: this is a permutation of independent blocks.
+// logical block xcd_block(nblocks) = (b % 8) * (grid / 8) + b / 8 gives every
+// XCD a contiguous range of logical blocks (rows); logical blocks >= nblocks
+// are idle and return at once.  Any mapping of workgroups to XCDs gives the
+// same results: this is a permutation of independent blocks.  The kernels
+// take nblocks as an argument and derive grid / 8 = ceil(nblocks / 8) from
+// it rather than reading the grid size: the explicit arguments arrive
+// preloaded in scalar registers (the library is built with kernel-argument
+// preloading), while the grid size would cost a memory round trip before a
+// wave's first request.
 inline unsigned xcd_grid(int64_t nblocks) { return (unsigned)(((nblocks + 7) / 8) * 8); }
 
-__device__ __forceinline__ int xcd_block() {
-  const int per = (int)(gridDim.x >> 3);
+__device__ __forceinline__ int xcd_block(int nblocks) {
+  const int per = (nblocks + 7) >> 3;
   const int b = (int)blockIdx.x;
   return (b & 7) * per + (b >> 3);
 }
@@ -83,6 +88,7 @@ struct LinearGroup {
   LinearCall call[kMaxGroup];
   int count;
   int blocks;  // logical blocks of all calls (the grid is rounded up to a multiple of 8)
+  int waves;   // matrix-core group: waves per block
 };
 
 // Launchers (return the HIP error of the launch; shapes already validated).

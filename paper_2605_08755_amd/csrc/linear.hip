@@ -682,30 +682,47 @@ __device__ __forceinline__ void flat_block_rpl(
   }
 }
 
+// The arguments every wave needs before its first memory request come first
+// (they arrive preloaded in scalar registers); y, needed only at the end,
+// comes last.
 template <int BITS, int MT, int NT, int RPL, int XB, bool SW>
 __global__ __launch_bounds__(NT) void linear_flat_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int nblocks) {
+    const uint8_t* __restrict__ zeros, int M, int N, int G, int R, float inv_g, int nblocks,
+    uint16_t* __restrict__ y) {
   // Slots of the XCD-rounded grid past nblocks get rows = 0 in flat_block (no
-  // early return: the argument loads then go out as one batch).
-  (void)nblocks;
+  // early return).
   if constexpr (RPL == 1)
-    flat_block<BITS, MT, NT, 1, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+    flat_block<BITS, MT, NT, 1, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(nblocks));
   else
-    flat_block_rpl<BITS, MT, NT, RPL, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block());
+    flat_block_rpl<BITS, MT, NT, RPL, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(nblocks));
 }
 
 // The same with the residual add + RMSNorm prologue (M = 1; no activation
 // pointer: the row is formed from np).
+// The first fourteen dwords of arguments (preloaded in scalar registers) are
+// what a wave needs before its first requests: the three prologue rows, the
+// weights, N and the packed shape gr = G | R << 8 (G <= 64, R <= 512); the
+// block count and fl(1/G) are derived from them.
 template <int NT, int RPL, bool SW, int BITS>
 __global__ __launch_bounds__(NT) void linear_flat_norm_kernel(
-    const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
-    uint16_t* __restrict__ y, int N, int G, int R, float inv_g, NormPrologue np) {
+    const float* __restrict__ res_in, const uint16_t* __restrict__ delta, const uint16_t* __restrict__ weight,
+    const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zeros, int N,
+    int gr, uint16_t* __restrict__ y, float* __restrict__ res_out, float eps) {
+  const int G = gr & 0xFF, R = gr >> 8;
+  const float inv_g = 1.0f / (float)G;  // correctly rounded, as the host's
+  const int nblocks = (N - 1) / R + 1;
+  NormPrologue np;
+  np.res_in = res_in;
+  np.delta = delta;
+  np.weight = weight;
+  np.res_out = res_out;
+  np.eps = eps;
   if constexpr (RPL == 1)
-    flat_block<BITS, 1, NT, 1, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(), np);
+    flat_block<BITS, 1, NT, 1, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(nblocks), np);
   else
-    flat_block_rpl<BITS, 1, NT, RPL, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(), np);
+    flat_block_rpl<BITS, 1, NT, RPL, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g,
+                                                  xcd_block(nblocks), np);
 }
 
 // Several independent calls in one launch: block b belongs to the last call
@@ -715,7 +732,7 @@ __global__ __launch_bounds__(NT) void linear_flat_norm_kernel(
 template <int BITS, int MT, int NT, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_group_kernel(const LinearGroup grp, int M) {
   // Slots past the last call's blocks fall to that call with rows = 0.
-  const int b = xcd_block();
+  const int b = xcd_block(grp.blocks);
   LinearCall c = grp.call[0];
 #pragma unroll
   for (int j = 1; j < kMaxGroup; ++j)
@@ -801,7 +818,7 @@ __global__ __launch_bounds__(kMlpThreads) void mlp_block_kernel(const MlpArgs a)
   float* pa = xsum + G1;                                  // [256 * G1] gate|up unit partials
   float* hsum = pa + 256 * G1;                            // [1]
 
-  const int b = xcd_block();
+  const int b = xcd_block(G2);
   if (b >= G2) return;  // XCD-rounding slot
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
@@ -1049,7 +1066,7 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
       const unsigned blocks = xcd_grid(nblocks);
 #define LAQ_FLAT_K(MTV, XBV, NTV, RPLV)                                                                     \
   launch(linear_flat_kernel<BITS, MTV, NTV, RPLV, XBV, false>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, \
-         ev, x, qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+         ev, x, qweight, scales, zeros, M, (int)N, G, R, 1.0f / (float)G, nblocks, y)
 #define LAQ_FLAT_NT(MTV, XBV, NTV)                       \
   do {                                                   \
     if (RPL == 2) LAQ_FLAT_K(MTV, XBV, NTV, 2);          \
@@ -1133,7 +1150,7 @@ hipError_t launch_linear_swiglu(const uint16_t* x, const uint32_t* qweight, cons
   const unsigned blocks = xcd_grid(nblocks);
 #define LAQ_SW_K(MTV, XBV, NTV)                                                                                   \
   launch(linear_flat_kernel<BITS, MTV, NTV, 1, XBV, true>, dim3(blocks), dim3(NTV), (uint32_t)lds, stream, ev, x, \
-         qweight, scales, zeros, y, M, (int)N, G, R, 1.0f / (float)G, nblocks)
+         qweight, scales, zeros, M, (int)N, G, R, 1.0f / (float)G, nblocks, y)
 #define LAQ_SW_NT(MTV, XBV)                 \
   do {                                      \
     if (NT == 512) LAQ_SW_K(MTV, XBV, 512); \
@@ -1183,8 +1200,8 @@ hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, c
   const int nblocks = (int)((N + R - 1) / R);
   const dim3 grid(xcd_grid(nblocks));
 #define LAQ_NORM_K(NTV, RPLV, SWV)                                                                                \
-  launch(linear_flat_norm_kernel<NTV, RPLV, SWV, BITS>, grid, dim3(NTV), (uint32_t)lds, stream, ev, qweight,      \
-         scales, zeros, y, (int)N, G, R, 1.0f / (float)G, np)
+  launch(linear_flat_norm_kernel<NTV, RPLV, SWV, BITS>, grid, dim3(NTV), (uint32_t)lds, stream, ev, np.res_in,     \
+         np.delta, np.weight, qweight, scales, zeros, (int)N, G | R << 8, y, np.res_out, np.eps)
   if (NT == 256) {
     if (swiglu) LAQ_NORM_K(256, 1, true);
     else if (RPL == 2) LAQ_NORM_K(256, 2, false);

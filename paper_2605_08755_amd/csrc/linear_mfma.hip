@@ -190,15 +190,24 @@ __device__ __forceinline__ void transpose_quarters(uint32_t& r0, uint32_t& r1, u
 constexpr int kSlabRowU4 = 64;          // one slab row: 64 pieces of 16 bytes
 constexpr int kBlockLdsU4 = 160 * 64;   // 160 KiB of LDS per block
 
+// Waves of a linear_mfma_kernel block: one per quad of the row, at most 8
+// (more waves per block measured slower: Qwen3-4B down, 19 quads, at M = 16
+// 10.3 us with 10 waves, 10.0 with 8) and as many M-row activation slabs
+// (M KiB each) as fit in 160 KiB; longer rows loop.  The host sizes the
+// block with it and the kernel derives its wave count from it.
+__host__ __device__ constexpr int mfma_block_waves(int M, int nq) {
+  const int wmax = 8 < kBlockLdsU4 / (M * kSlabRowU4) ? 8 : kBlockLdsU4 / (M * kSlabRowU4);
+  return wmax < nq ? wmax : nq;
+}
+
 template <int BITS, int TW>
 __device__ __forceinline__ void mfma_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block) {
+    const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int block, int W) {
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ u32x4 wslabs[];  // [W][M rows][64 pieces]; afterwards the wave's partials
 
   const int K = 128 * G;
-  const int W = (int)(blockDim.x >> 6);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar loop
   const int nl = lane & 15;  // weight row of a tile / activation row / result column
@@ -307,7 +316,7 @@ __device__ __forceinline__ void mfma_block(
 #pragma unroll
     for (int r = 0; r < 4; ++r) red[wave * kWaveSlabF + (t * 4 + r) * 64 + lane] = yacc[t][r];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < TW * 4 * 64; idx += blockDim.x) {
+  for (int idx = threadIdx.x; idx < TW * 4 * 64; idx += 64 * W) {
     const int t = idx >> 8;
     const int r = (idx >> 6) & 3;
     const int ln = idx & 63;
@@ -506,7 +515,7 @@ template <int BITS, int TB>
 __global__ __launch_bounds__(64 * TB) void linear_mfma_tiles_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
-  const int block = xcd_block();
+  const int block = xcd_block(nblocks);
   if (block >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
   mfma_tiles_block<BITS, TB>(x, qw, scales, zeros, y, M, N, G, block);
 }
@@ -644,7 +653,7 @@ __global__ __launch_bounds__(64 * kFullTiles) void linear_mfma_split_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, float* __restrict__ part, int M, int N, int G, int tile_blocks,
     int nblocks) {
-  const int b = xcd_block();
+  const int b = xcd_block(nblocks);
   if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
   const int sidx = b / tile_blocks;
   mfma_full_block<BITS, NQ>(x, qw, scales, zeros, nullptr, M, N, G, b - sidx * tile_blocks, sidx * NQ,
@@ -691,22 +700,22 @@ template <int BITS, int TW>
 __global__ __launch_bounds__(1024 / TW) void linear_mfma_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int nblocks) {
-  const int block = xcd_block();
+  const int block = xcd_block(nblocks);
   if (block >= nblocks) return;  // idle slot of the XCD-rounded grid
-  mfma_block<BITS, TW>(x, qw, scales, zeros, y, M, N, G, block);
+  mfma_block<BITS, TW>(x, qw, scales, zeros, y, M, N, G, block, mfma_block_waves(M, (G + 3) >> 2));
 }
 
 // Several independent calls in one launch (one 16-row tile per block); the
 // call of block b is picked with constant indices, as in the flat kernel.
 template <int BITS>
 __global__ __launch_bounds__(1024) void linear_mfma_group_kernel(const LinearGroup grp, int M) {
-  const int b = xcd_block();
+  const int b = xcd_block(grp.blocks);
   if (b >= grp.blocks) return;  // idle slot of the XCD-rounded grid
   LinearCall c = grp.call[0];
 #pragma unroll
   for (int j = 1; j < kMaxGroup; ++j)
     if (j < grp.count && b >= grp.call[j].first_block) c = grp.call[j];
-  mfma_block<BITS, 1>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, b - c.first_block);
+  mfma_block<BITS, 1>(c.x, c.qw, c.scales, c.zeros, c.y, M, c.N, c.G, b - c.first_block, grp.waves);
 }
 
 // ---------------------------------------------------------------------------
@@ -744,10 +753,10 @@ linear_mfma_quad_wave_kernel(
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ u32x4 wslab[];  // [W][MT rows][64 pieces]; afterwards [W][4][64] fp32 partials
   constexpr int WL = BITS + 2;      // weight loads per lane
-  const int b = xcd_block();
+  const int b = xcd_block(nblocks);
   if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
   const int K = 128 * G;
-  const int W = (int)(blockDim.x >> 6);
+  const int W = (G + 3) >> 2;  // one wave per quad (the block size)
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // this wave's quad
   const int nl = lane & 15;  // weight row / activation row / result column
@@ -849,7 +858,7 @@ linear_mfma_quad_wave_kernel(
   //    Lane (n, j) of a wave held rows m = 4j .. 4j+3 of column n.
   const float* red = reinterpret_cast<const float*>(wslab);
   const int wstride = MT * 64 * 4;  // floats per wave region
-  for (int idx = threadIdx.x; idx < 256; idx += blockDim.x) {
+  for (int idx = threadIdx.x; idx < 256; idx += 64 * W) {
     const int r = idx >> 6;
     const int ln = idx & 63;
     float v = 0.0f;
@@ -881,7 +890,7 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8))) void 
   typedef __attribute__((address_space(3))) void lds_void;
   extern __shared__ u32x4 wslab[];  // [nq][MT rows][64 pieces]; afterwards [TPB * nq][4][64] fp32 partials
   constexpr int WL = BITS + 2;
-  const int b = xcd_block();
+  const int b = xcd_block(nblocks);
   if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
   const int K = 128 * G;
   const int nq = (G + 3) / 4;
@@ -971,7 +980,7 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8))) void 
 
   // 3. Outputs of each tile: its nq waves' partials in quad order.
   const float* red = reinterpret_cast<const float*>(wslab);
-  for (int idx = threadIdx.x; idx < 256 * TPB; idx += blockDim.x) {
+  for (int idx = threadIdx.x; idx < 256 * TPB; idx += 64 * TPB * nq) {
     const int tt = idx >> 8;
     const int r = (idx >> 6) & 3;
     const int ln = idx & 63;
@@ -1096,12 +1105,7 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
   // keep a block on every compute unit (measured on MI355X).  (At most M
   // tiles per wave: a wave's TW KiB of partials reuse its M KiB slab.)
   const int TW = min(M, (tiles >= 256 && G >= 32) ? 2 : 1);
-  // One wave per quad of the row, at most 8 (more waves per block measured
-  // slower: Qwen3-4B down, 19 quads, at M = 16 10.3 us with 10 waves, 10.0
-  // with 8) and as many M-row activation slabs (M KiB each) as fit in
-  // 160 KiB; longer rows loop.
-  const int wmax = min(8, kBlockLdsU4 / (M * kSlabRowU4));
-  const int W = min(wmax, nq);
+  const int W = mfma_block_waves(M, nq);
   const int nblocks = (int)((tiles + TW - 1) / TW);
   const unsigned blocks = xcd_grid(nblocks);
   const uint32_t lds = (uint32_t)W * M * kSlabRowU4 * 16;
@@ -1130,7 +1134,8 @@ hipError_t launch_linear_mfma_group(LinearCall* calls, int count, int M, hipStre
   }
   grp.count = count;
   grp.blocks = (int)blocks;
-  const int W = min(min(8, kBlockLdsU4 / (M * kSlabRowU4)), nq_max);  // as for one call
+  const int W = mfma_block_waves(M, nq_max);  // as for one call
+  grp.waves = W;
   launch(linear_mfma_group_kernel<BITS>, dim3(xcd_grid(blocks)), dim3(64 * W), (uint32_t)W * M * kSlabRowU4 * 16,
          stream, ev, grp, M);
   return hipGetLastError();
