@@ -572,7 +572,8 @@ def summarize_trace(path, launches, steps):
         sums.append(sum(durs[i * launches:(i + 1) * launches]))
     by = {}
     for r, d in zip(rows, durs):
-        key = (r["Kernel_Name"].split("(")[0][-60:], r.get("Grid_Size_X", r.get("Grid_Size", "")))
+        name = r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("void ", "")
+        key = (name.split("(")[0][-60:], r.get("Grid_Size_X", r.get("Grid_Size", "")))
         by.setdefault(key, []).append(d)
     med = lambda v: sorted(v)[len(v) // 2]
     lines = ["| kernel (name tail) | grid | dispatches | avg µs | p50 µs | min µs |", "|---|---|---|---|---|---|"]
