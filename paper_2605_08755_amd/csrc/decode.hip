@@ -113,15 +113,19 @@ __global__ __launch_bounds__(kNormThreads) void add_rmsnorm_kernel(float* __rest
 // RMSNorm of one 128-value head held by a wave (lane i: dimensions i and
 // i + 64, a and b) with weights wn, then the rotary embedding of the pair
 // (a, b) by the angle whose cosine and sine are cs[i] and cs[64 + i].
-__device__ __forceinline__ void norm_rope_pair(float& a, float& b, const uint16_t* __restrict__ wn,
-                                               const float* __restrict__ cs, float eps, int i) {
+// The same with the lane's norm weights (wa, wb) and rotation (c, s) given.
+__device__ __forceinline__ void norm_rope_vals(float& a, float& b, float wa, float wb, float c, float s, float eps) {
   const float ss = wave_sum(fmaf(a, a, b * b));
   const float inv = 1.0f / sqrtf(ss / (float)kHeadDim + eps);
-  const float na = a * inv * h2f(wn[i]);
-  const float nb = b * inv * h2f(wn[i + 64]);
-  const float c = cs[i], s = cs[64 + i];
+  const float na = a * inv * wa;
+  const float nb = b * inv * wb;
   a = na * c - nb * s;
   b = nb * c + na * s;
+}
+
+__device__ __forceinline__ void norm_rope_pair(float& a, float& b, const uint16_t* __restrict__ wn,
+                                               const float* __restrict__ cs, float eps, int i) {
+  norm_rope_vals(a, b, h2f(wn[i]), h2f(wn[i + 64]), cs[i], cs[64 + i], eps);
 }
 
 // One head per block (64 lanes; lane i holds dimensions i and i + 64, the
@@ -325,8 +329,8 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(const float* __restric
 template <int R, int P>
 __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
     uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int S_max, int pos, const uint16_t* __restrict__ qkv,
-    const uint16_t* __restrict__ qw, const float* __restrict__ cs, float eps, int Hq, int Hkv,
-    const uint16_t* __restrict__ kw, int T, float* __restrict__ ws) {
+    const uint16_t* __restrict__ qw, const float* __restrict__ cs, float eps, int Hq,
+    const uint16_t* __restrict__ kw, int Hkv, int T, float* __restrict__ ws) {
   static_assert(P == 16 || P == 32 || P == 64, "tile of 16, 32 or 64 positions");
   constexpr int DS = 64 / P;                   // lanes per position (dimension slices)
   constexpr int kUnits = P * kHeadDim / 8;     // 16-byte units of keys (and of values) per tile
@@ -355,37 +359,45 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
     ka[i] = __builtin_amdgcn_raw_buffer_load_b128(kr, u * 16, 0, 0);
     va[i] = __builtin_amdgcn_raw_buffer_load_b128(vr, u * 16, 0, 0);
   }
-  // this wave's query head (and, in the block holding pos, wave 0: the new key and value)
+  __builtin_amdgcn_sched_barrier(0);  // the tile's loads go out first
+  // This wave's query head, its norm weights and the rotation of pos; then
+  // the new token's key and value of head g with the key norm weights, which
+  // only wave 0 of the block holding pos uses: every wave loads them (a few
+  // bytes) because a load under a branch would be waited for inside it,
+  // putting a second round trip on that block's path.
   const uint16_t* qsrc = qkv + (int64_t)(g * R + w) * kHeadDim;
-  float a = h2f(qsrc[lane]), b = h2f(qsrc[lane + 64]);
+  const uint16_t* ksrc = qkv + (int64_t)(Hq + g) * kHeadDim;
+  const uint16_t qa = qsrc[lane], qb = qsrc[lane + 64];
+  const uint16_t wqa = qw[lane], wqb = qw[lane + 64];
+  const float rc = cs[lane], rs = cs[64 + lane];
+  const uint16_t kra = ksrc[lane], krb = ksrc[lane + 64];
+  __builtin_amdgcn_sched_barrier(0);  // then these, before the loads that wait for kw and Hkv
+  const uint16_t wka = kw[lane], wkb = kw[lane + 64];
+  const uint16_t* vsrc = ksrc + (int64_t)Hkv * kHeadDim;
+  const uint16_t v0 = vsrc[lane], v1 = vsrc[lane + 64];
   const bool own = pos >= p0 && pos < p0 + P;  // uniform over the block
-  float ka0 = 0.0f, kb0 = 0.0f;
-  uint16_t v0 = 0, v1 = 0;
-  if (own && w == 0) {
-    const uint16_t* ksrc = qkv + (int64_t)(Hq + g) * kHeadDim;
-    const uint16_t* vsrc = qkv + (int64_t)(Hq + Hkv + g) * kHeadDim;
-    ka0 = h2f(ksrc[lane]);
-    kb0 = h2f(ksrc[lane + 64]);
-    v0 = vsrc[lane];
-    v1 = vsrc[lane + 64];
-  }
-  norm_rope_pair(a, b, qw, cs, eps, lane);
+  float a = h2f(qa), b = h2f(qb);
+  norm_rope_vals(a, b, h2f(wqa), h2f(wqb), rc, rs, eps);
   uint16_t* qh16 = reinterpret_cast<uint16_t*>(qh[w]);
   qh16[lane] = f2h(a);
   qh16[lane + 64] = f2h(b);
-  // Rows past nload were read as zeros (buffer extent); every row but the new
-  // token's (written below) is staged, so the tile holds finite values only.
-  const int own_row = own ? pos - p0 : -1;
+  // Rows past nload were read as zeros (buffer extent), so the tile holds
+  // finite values only; in the block holding pos, wave 0 then overwrites the
+  // new token's row (zeros here) after a barrier.  (Staging every row, with no
+  // test of the row, keeps the compiler from sinking the tile's loads into a
+  // conditional store, behind the query's round trip.)
 #pragma unroll
   for (int i = 0; i < kPer; ++i) {
     const int u = i * kThreads + tid;
-    if (u < kUnits && (u >> 4) != own_row) {
+    if (kPer * kThreads == kUnits || u < kUnits) {
       kt[(u >> 4) * kKeyStrideU4 + (u & 15)] = ka[i];
       vt[u] = va[i];
     }
   }
+  if (own) __syncthreads();  // uniform over the block
   if (own && w == 0) {
-    norm_rope_pair(ka0, kb0, kw, cs, eps, lane);
+    float ka0 = h2f(kra), kb0 = h2f(krb);
+    norm_rope_vals(ka0, kb0, h2f(wka), h2f(wkb), rc, rs, eps);
     const uint16_t k0 = f2h(ka0), k1 = f2h(kb0);
     const int64_t crow = ((int64_t)g * S_max + pos) * kHeadDim;
     kc[crow + lane] = k0;
@@ -597,7 +609,7 @@ hipError_t launch_decode_attention_qkv(const uint16_t* qkv, const uint16_t* qw, 
   const float* cs = cos_sin + pos * kHeadDim;
 #define LAQ_ATTN_QKV(RV, PV)                                                                                 \
   launch(attn_qkv_partial_kernel<RV, PV>, grid, dim3(64 * RV), 0, stream, e1, kc, vc, (int)S_max, (int)pos, qkv, \
-         qw, cs, eps, (int)Hq, (int)Hkv, kw, T, ws)
+         qw, cs, eps, (int)Hq, kw, (int)Hkv, T, ws)
 #define LAQ_ATTN_QKV_P(RV)                 \
   do {                                     \
     if (P == 64) LAQ_ATTN_QKV(RV, 64);     \
