@@ -375,6 +375,8 @@ __global__ __launch_bounds__(64 * R) void attn_qkv_partial_kernel(
   const uint16_t wka = kw[lane], wkb = kw[lane + 64];
   const uint16_t* vsrc = ksrc + (int64_t)Hkv * kHeadDim;
   const uint16_t v0 = vsrc[lane], v1 = vsrc[lane + 64];
+  // T and ws follow the preloaded arguments: read them now, not at the end.
+  asm volatile("" : "+s"(T), "+s"(ws));
   const bool own = pos >= p0 && pos < p0 + P;  // uniform over the block
   float a = h2f(qa), b = h2f(qb);
   norm_rope_vals(a, b, h2f(wqa), h2f(wqb), rc, rs, eps);

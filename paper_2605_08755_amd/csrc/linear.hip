@@ -425,6 +425,17 @@ __device__ __forceinline__ void swiglu_rows(const float* part, int R, int G, int
   }
 }
 
+// A value held in scalar registers from the point of the call on: the "+s"
+// operand keeps the compiler from re-reading a kernel argument where it is
+// used.  Arguments past the preloaded ones (the output pointer, the norm's
+// eps and residual output) are pinned right after a block issues its loads,
+// so their scalar round trip overlaps the loads instead of sitting at the
+// end of the block's critical path.
+template <typename T>
+__device__ __forceinline__ void pin_sgpr(T& v) {
+  asm volatile("" : "+s"(v));
+}
+
 // One block of the flat kernel: rows block*R .. block*R + R - 1 of one call.
 // Thread t takes units t + i*NT (i < UPT) of each pass over the block's
 // units; every launch uses UPT = 1 (more units per thread measured slower).
@@ -492,9 +503,15 @@ __device__ __forceinline__ void flat_block(
     }
   }
   __builtin_amdgcn_sched_barrier(0);
+  uint16_t* const yo = [&] { uint16_t* p = y; pin_sgpr(p); return p; }();
+  NormPrologue npl = np;
+  if constexpr (NORM) {
+    pin_sgpr(npl.eps);
+    pin_sgpr(npl.res_out);
+  }
 
   // 3. Stage activations and per-group sums (first pass from the loads above).
-  if constexpr (NORM) norm_finish<XB, NT>(nl_, np, 128 * G, t, block == 0, xv);
+  if constexpr (NORM) norm_finish<XB, NT>(nl_, npl, 128 * G, t, block == 0, xv);
   stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);
   for (int base = XB * NT; !NORM && base < XU; base += XB * NT) {
 #pragma unroll
@@ -568,7 +585,7 @@ __device__ __forceinline__ void flat_block(
   // 5. Row sums in a fixed order: lane l of a row's 16 adds groups l, l+16, ...
   const int l = t & 15;
   if constexpr (SW) {
-    swiglu_rows<MT, NT>(part, R, G, rows, M, N, row0, y, t);
+    swiglu_rows<MT, NT>(part, R, G, rows, M, N, row0, yo, t);
   } else {
     for (int rr = t >> 4; rr < rows; rr += NT / 16) {
 #pragma unroll
@@ -576,7 +593,7 @@ __device__ __forceinline__ void flat_block(
         float acc = 0.0f;
         for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
         acc = row16_sum(acc);
-        if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+        if (l == 0 && m < M) yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
       }
     }
   }
@@ -638,9 +655,15 @@ __device__ __forceinline__ void flat_block_rpl(
 #pragma unroll
   for (int i = 0; i < RPL; ++i) load_flat_unit<BITS>(qr, sr, zr, rb + i * R1, g0, G, wv[i], sv[i], zv[i]);
   __builtin_amdgcn_sched_barrier(0);
+  uint16_t* const yo = [&] { uint16_t* p = y; pin_sgpr(p); return p; }();
+  NormPrologue npl = np;
+  if constexpr (NORM) {
+    pin_sgpr(npl.eps);
+    pin_sgpr(npl.res_out);
+  }
 
   // 2. Stage activations and per-group sums (first pass from the loads above).
-  if constexpr (NORM) norm_finish<XB, NT>(nl_, np, 128 * G, t, block == 0, xv);
+  if constexpr (NORM) norm_finish<XB, NT>(nl_, npl, 128 * G, t, block == 0, xv);
   stage_x_pass<MT, NT, XB>(xv, 0, t, XU, xl, xsum);
   for (int base = XB * NT; !NORM && base < XU; base += XB * NT) {
 #pragma unroll
@@ -668,7 +691,7 @@ __device__ __forceinline__ void flat_block_rpl(
   // 4. Row sums in a fixed order: lane l of a row's 16 adds groups l, l+16, ...
   const int l = t & 15;
   if constexpr (SW) {
-    swiglu_rows<MT, NT>(part, R, G, rows, M, N, row0, y, t);
+    swiglu_rows<MT, NT>(part, R, G, rows, M, N, row0, yo, t);
   } else {
     for (int rr = t >> 4; rr < rows; rr += NT / 16) {
 #pragma unroll
@@ -676,7 +699,7 @@ __device__ __forceinline__ void flat_block_rpl(
         float acc = 0.0f;
         for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
         acc = row16_sum(acc);
-        if (l == 0 && m < M) y[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+        if (l == 0 && m < M) yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
       }
     }
   }

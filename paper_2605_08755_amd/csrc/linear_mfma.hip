@@ -584,6 +584,7 @@ __device__ __forceinline__ void mfma_full_block(
     __builtin_amdgcn_sched_barrier(0);
   };
   static_for<D>(issue);
+  asm volatile("" : "+s"(part));  // an argument past the preloaded ones: read it now, not at the end
 
   // 2. Quad by quad: wait until only the later quads' loads are outstanding,
   //    a bare barrier (the other waves' slab rows; a __syncthreads() fence
@@ -651,8 +652,8 @@ __device__ __forceinline__ void mfma_full_block(
 template <int BITS, int NQ>
 __global__ __launch_bounds__(64 * kFullTiles) void linear_mfma_split_kernel(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, float* __restrict__ part, int M, int N, int G, int tile_blocks,
-    int nblocks) {
+    const uint8_t* __restrict__ zeros, int M, int N, int G, int tile_blocks, int nblocks,
+    float* __restrict__ part) {
   const int b = xcd_block(nblocks);
   if (b >= nblocks) return;  // idle slot of the XCD-rounded grid (the whole block leaves)
   const int sidx = b / tile_blocks;
@@ -1089,11 +1090,11 @@ hipError_t launch_linear_mfma(const uint16_t* x, const uint32_t* qweight, const 
     const dim3 grid(xcd_grid(nblocks)), blk(64 * kFullTiles);
     const uint32_t lds = (uint32_t)sp.qs * kSlabBytes;
     switch (sp.qs) {
-      case 1: launch(linear_mfma_split_kernel<BITS, 1>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
-      case 2: launch(linear_mfma_split_kernel<BITS, 2>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
-      case 3: launch(linear_mfma_split_kernel<BITS, 3>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
-      case 4: launch(linear_mfma_split_kernel<BITS, 4>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
-      default: launch(linear_mfma_split_kernel<BITS, 5>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, workspace, M, (int)N, G, sp.tile_blocks, nblocks); break;
+      case 1: launch(linear_mfma_split_kernel<BITS, 1>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, M, (int)N, G, sp.tile_blocks, nblocks, workspace); break;
+      case 2: launch(linear_mfma_split_kernel<BITS, 2>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, M, (int)N, G, sp.tile_blocks, nblocks, workspace); break;
+      case 3: launch(linear_mfma_split_kernel<BITS, 3>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, M, (int)N, G, sp.tile_blocks, nblocks, workspace); break;
+      case 4: launch(linear_mfma_split_kernel<BITS, 4>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, M, (int)N, G, sp.tile_blocks, nblocks, workspace); break;
+      default: launch(linear_mfma_split_kernel<BITS, 5>, grid, blk, lds, stream, e1, x, qweight, scales, zeros, M, (int)N, G, sp.tile_blocks, nblocks, workspace); break;
     }
     const int64_t MN = (int64_t)M * N;
     launch(splitk_reduce_kernel, dim3((unsigned)((MN + 1023) / 1024)), dim3(256), 0, stream, e2,
