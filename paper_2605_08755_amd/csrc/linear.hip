@@ -452,9 +452,11 @@ __device__ __forceinline__ void flat_block(
 
   const int t = threadIdx.x;
   // An idle block (an XCD-rounding slot past the last row) has rows = 0: every
-  // buffer extent is zero, so it loads and stores nothing.
-  const int64_t row0 = (int64_t)block * R;
-  const int rows = (int)max((int64_t)0, min((int64_t)R, (int64_t)N - row0));
+  // buffer extent is zero, so it loads and stores nothing.  (32-bit unsigned
+  // scalar arithmetic: block * R < N + 8R < 2^32.)
+  const uint32_t r0u = (uint32_t)block * (uint32_t)R;
+  const int rows = r0u < (uint32_t)N ? (int)min((uint32_t)R, (uint32_t)N - r0u) : 0;
+  const int64_t row0 = (int64_t)r0u;
   const int U = rows * G;
   const int XU = MT * G * 16;  // activation tile in 16-byte units (rows m >= M read as zero)
 
@@ -463,12 +465,11 @@ __device__ __forceinline__ void flat_block(
   const __amdgpu_buffer_rsrc_t sr = make_rsrc(scales + row0 * G, (uint32_t)U * 2);
   const __amdgpu_buffer_rsrc_t zr = make_rsrc(zeros + row0 * G, (uint32_t)U);
 
-  // Unit t + i*NT is (row r, group g); (r, g) advance by (NT / G, NT % G)
-  // per step.  Computed before any load so that no load waits on it.
-  // t / G as trunc((t + 0.5) * fl(1/G)): the quotient's fractional part is at
-  // least 0.5/G away from an integer and the float error is below 1025 * 2^-23 / G,
-  // so the truncation is exact for every t < 1024 and G >= 1.
-  const int dr = NT / G, dg = NT - (NT / G) * G;
+  // Unit t + i*NT is (row r, group g).  Computed before any load so that no
+  // load waits on it.  t / G as trunc((t + 0.5) * fl(1/G)): the quotient's
+  // fractional part is at least 0.5/G away from an integer and the float
+  // error is below 1025 * 2^-23 / G, so the truncation is exact for every
+  // t < 1024 and G >= 1.
   const int r0 = (int)(((float)t + 0.5f) * inv_g);
   const int g0 = t - r0 * G;
   __builtin_amdgcn_sched_barrier(0);
@@ -497,9 +498,11 @@ __device__ __forceinline__ void flat_block(
     for (int i = 0; i < UPT; ++i) {
       load_flat_unit<BITS>(qr, sr, zr, r, g, G, wv[i], sv[i], zv[i]);
       gi[i] = g;
-      g += dg;
-      r += dr;
-      if (g >= G) { g -= G; r += 1; }
+      if (i + 1 < UPT) {  // (r, g) advance by (NT / G, NT % G)
+        g += NT % G;
+        r += NT / G;
+        if (g >= G) { g -= G; r += 1; }
+      }
     }
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -521,7 +524,9 @@ __device__ __forceinline__ void flat_block(
   }
   __syncthreads();
 
-  // 4. Units: one 128-group of one row each.
+  // 4. Units: one 128-group of one row each ((r, g) advance by (NT / G,
+  //    NT % G) per unit step; every launch has R * G <= NT, one pass).
+  const int dr = NT / G, dg = NT - (NT / G) * G;
   int ur = r0, ug = g0;
   for (int ub = 0; ub < U; ub += UPT * NT) {
     if (ub > 0) {
@@ -615,9 +620,11 @@ __device__ __forceinline__ void flat_block_rpl(
 
   const int t = threadIdx.x;
   // An idle block (an XCD-rounding slot past the last row) has rows = 0: every
-  // buffer extent is zero, so it loads and stores nothing.
-  const int64_t row0 = (int64_t)block * R;
-  const int rows = (int)max((int64_t)0, min((int64_t)R, (int64_t)N - row0));
+  // buffer extent is zero, so it loads and stores nothing.  (32-bit unsigned
+  // scalar arithmetic: block * R < N + 8R < 2^32.)
+  const uint32_t r0u = (uint32_t)block * (uint32_t)R;
+  const int rows = r0u < (uint32_t)N ? (int)min((uint32_t)R, (uint32_t)N - r0u) : 0;
+  const int64_t row0 = (int64_t)r0u;
   const int U = rows * G;
   const int XU = MT * G * 16;  // activation tile in 16-byte units (rows m >= M read as zero)
   const int R1 = R / RPL;
