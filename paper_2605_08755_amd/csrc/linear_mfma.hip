@@ -212,8 +212,11 @@ __device__ __forceinline__ void mfma_block(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar loop
   const int nl = lane & 15;  // weight row of a tile / activation row / result column
   const int q = lane >> 4;   // load: group of the quad; compute: chunk of the group
-  const int64_t row0 = (int64_t)block * (16 * TW);
-  const int rows = (int)min((int64_t)16 * TW, (int64_t)N - row0);
+  // Row range in 32-bit unsigned scalar arithmetic (row0 < N + 2^10 < 2^32):
+  // 64-bit compares would run on the vector unit ahead of the first load.
+  const uint32_t r0u = (uint32_t)block * (16u * TW);
+  const int64_t row0 = (int64_t)r0u;
+  const int rows = r0u < (uint32_t)N ? (int)min(16u * TW, (uint32_t)N - r0u) : 0;
   const int C = 4 * G;
   const int nq = (G + 3) >> 2;
   u32x4* const sl = wslabs + wave * (M * kSlabRowU4);
@@ -394,8 +397,9 @@ __device__ __forceinline__ void mfma_tiles_block(
   const int nl = lane & 15;  // weight row / activation row / result column
   const int j = lane >> 4;   // load: group of the quad; compute: chunk of the group
   const int nq = (G + 3) >> 2;
-  const int64_t row0 = ((int64_t)block * TB + wave) * 16;
-  const int rows = (int)max((int64_t)0, min((int64_t)16, (int64_t)N - row0));
+  const uint32_t r0u = ((uint32_t)block * TB + (uint32_t)wave) * 16u;  // 32-bit: see mfma_block
+  const int64_t row0 = (int64_t)r0u;
+  const int rows = r0u < (uint32_t)N ? (int)min(16u, (uint32_t)N - r0u) : 0;
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
   const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * 4 * G, (uint32_t)rows * BITS * G * 16);  // 16 B per plane-group
@@ -549,8 +553,9 @@ __device__ __forceinline__ void mfma_full_block(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform: scalar descriptors
   const int nl = lane & 15;  // weight row / activation row / result column
   const int j = lane >> 4;   // load: group of the quad; compute: chunk of the group
-  const int64_t row0 = ((int64_t)block * kFullTiles + wave) * 16;
-  const int rows = (int)max((int64_t)0, min((int64_t)16, (int64_t)N - row0));
+  const uint32_t r0u = ((uint32_t)block * kFullTiles + (uint32_t)wave) * 16u;  // 32-bit: see mfma_block
+  const int64_t row0 = (int64_t)r0u;
+  const int rows = r0u < (uint32_t)N ? (int)min(16u, (uint32_t)N - r0u) : 0;
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
   const __amdgpu_buffer_rsrc_t qr = rsrc(qw + row0 * BITS * 4 * G, (uint32_t)rows * BITS * G * 16);
@@ -762,8 +767,9 @@ linear_mfma_quad_wave_kernel(
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // this wave's quad
   const int nl = lane & 15;  // weight row / activation row / result column
   const int j = lane >> 4;   // load: group of the quad; compute: chunk of the group
-  const int64_t row0 = (int64_t)b * 16;
-  const int rows = (int)min((int64_t)16, (int64_t)N - row0);
+  const uint32_t r0u = (uint32_t)b * 16u;  // 32-bit: see mfma_block
+  const int64_t row0 = (int64_t)r0u;
+  const int rows = r0u < (uint32_t)N ? (int)min(16u, (uint32_t)N - r0u) : 0;
   u32x4* const sl = wslab + wave * (MT * 64);
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
@@ -901,8 +907,9 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(8))) void 
   const int q = w - t * nq;                              // quad of the row
   const int nl = lane & 15;
   const int j = lane >> 4;
-  const int64_t row0 = ((int64_t)b * TPB + t) * 16;
-  const int rows = (int)max((int64_t)0, min((int64_t)16, (int64_t)N - row0));
+  const uint32_t r0u = ((uint32_t)b * TPB + (uint32_t)t) * 16u;  // 32-bit: see mfma_block
+  const int64_t row0 = (int64_t)r0u;
+  const int rows = r0u < (uint32_t)N ? (int)min(16u, (uint32_t)N - r0u) : 0;
   u32x4* const sl = wslab + q * (MT * 64);
 
   const __amdgpu_buffer_rsrc_t xr = rsrc(x, (uint32_t)M * K * 2);
