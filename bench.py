@@ -296,7 +296,9 @@ def decode_step_extra(stack, dev, steps, context=1024):
     context - 1, captured in a HIP graph.  Variants: W3 linears and a W3 LM
     head; W3 with the gate|up + SiLU linear and a W3 or an fp16 LM head; the
     same with the norms before q|k|v and gate|up inside those linears
-    (laq.add_rmsnorm_linear); fp16 weights everywhere through torch's dense
+    (laq.add_rmsnorm_linear), also with o and down adding their outputs to
+    the residual stream (laq.linear_residual) and with the MLP block in one
+    launch (laq.add_rmsnorm_mlp); fp16 weights everywhere through torch's dense
     GEMM (the unquantized reference).  The paper does not say whether its decoding benchmark
     quantizes the LM head, hence both heads.  Attention is the fused
     q/k-norm + rotary + attention call except in the _separate_attention
@@ -352,6 +354,16 @@ def decode_step_extra(stack, dev, steps, context=1024):
         f = w3_lin(i)
         return with_norm(f, *stack.q[3][i]) if i % 4 == 0 else f
 
+    def w3_residual_lin(i):
+        # as w3_norm_lin, with o and down adding their outputs to the residual
+        # stream themselves (laq.linear_residual), so the norms take no delta
+        f = w3_norm_lin(i)
+        if i % 4 in (1, 3):
+            q, sc, z = stack.q[3][i]
+            f.residual_linear = lambda x, r_in, r_out, out: laq.linear_residual(x, q, sc, z, r_in, r_out, 3,
+                                                                                out=out)
+        return f
+
     mlp_ws = laq.mlp_workspace(D, I, dev)  # stream-ordered calls share it
 
     def w3_merged_mlp_lin(i):
@@ -371,6 +383,7 @@ def decode_step_extra(stack, dev, steps, context=1024):
     out = {"context": context, "layers": shape["layers"], "vocab": V}
     variants = (("w3", w3_lin, head_w3, True), ("w3_fused_swiglu", w3_swiglu_lin, head_w3, True),
                 ("w3_fused_swiglu_fused_norms", w3_norm_lin, head_w3, True),
+                ("w3_fused_norms_residual", w3_residual_lin, head_w3, True),
                 ("w3_merged_mlp", w3_merged_mlp_lin, head_w3, True),
                 ("w3_fused_swiglu_separate_attention", w3_swiglu_lin, head_w3, False),
                 ("w3_fused_swiglu_fp16_head", w3_swiglu_lin, head_fp16, True), ("fp16", fp16_lin, head_fp16, True))
@@ -383,7 +396,8 @@ def decode_step_extra(stack, dev, steps, context=1024):
         out[name] = {"us": round(ms * 1e3, 1), "tokens_per_s": round(1e3 / ms, 1)}
         del step
     swiglu_w.clear()
-    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fused_norms", "w3_merged_mlp", "w3_fused_swiglu_fp16_head"):
+    for name in ("w3", "w3_fused_swiglu", "w3_fused_swiglu_fused_norms", "w3_fused_norms_residual", "w3_merged_mlp",
+                 "w3_fused_swiglu_fp16_head"):
         out[name + "_speedup_vs_fp16"] = round(out["fp16"]["us"] / out[name]["us"], 3)
 
     # Attention alone: a HIP graph of the 36 layers' attention calls (each

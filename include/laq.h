@@ -368,6 +368,30 @@ laq_status laq_add_rmsnorm_linear_swiglu_w4g128(const float *residual, const voi
                                                 const uint8_t *zeros, void *y, int64_t N, int64_t K,
                                                 void *stream);
 
+/* laq_linear_residual_w3g128 -- a batch-1 linear that also updates the
+ * residual stream: y = x w_hat^T exactly as laq_linear_w3g128 with M = 1
+ * (Eq. 1 dequantization, App. H format; bit for bit the same y), and
+ *   residual_out[n] = residual_in[n] + y[n]      (fp32 + the fp16 output)
+ * for every output row n (the decode step's o and down projections, whose
+ * outputs the residual stream adds; Sec. 5, Table 3 setting).  The next
+ * norm then reads the new residual with no delta (laq_add_rmsnorm_linear_*
+ * with delta NULL).
+ *   x, qweight, scales, zeros, y, N, K  as laq_linear_w3g128 with M = 1.
+ *   residual_in   [in] fp32 [N], 4-byte aligned.
+ *   residual_out  [out] fp32 [N], 4-byte aligned; may be residual_in itself
+ *                 (in place), otherwise must not overlap it.
+ * Errors: NULL_POINTER; BAD_SHAPE (shape rules of laq_linear_w3g128, K below
+ * 2048, rows too long for one activation tile in LDS (K above about 28000),
+ * partial overlap of the residuals); MISALIGNED. */
+laq_status laq_linear_residual_w3g128(const void *x, const uint32_t *qweight, const void *scales,
+                                      const uint8_t *zeros, void *y, const float *residual_in,
+                                      float *residual_out, int64_t N, int64_t K, void *stream);
+
+/* W4G128 sibling (qweight as laq_linear_w4g128). */
+laq_status laq_linear_residual_w4g128(const void *x, const uint32_t *qweight, const void *scales,
+                                      const uint8_t *zeros, void *y, const float *residual_in,
+                                      float *residual_out, int64_t N, int64_t K, void *stream);
+
 /* laq_mlp_workspace_bytes -- device workspace (bytes) that
  * laq_add_rmsnorm_mlp_w3g128 needs for hidden size D and MLP width I
  * (fp32 partial sums per 128 intermediates, fp32 team sums, counters);

@@ -399,6 +399,29 @@ laq_status norm_linear(const char* fn, const float* residual, const void* delta,
 }
 
 template <int BITS>
+laq_status linear_residual(const char* fn, const void* x, const uint32_t* qweight, const void* scales,
+                           const uint8_t* zeros, void* y, const float* residual_in, float* residual_out, int64_t N,
+                           int64_t K, void* stream) {
+  const laq::LaunchEvents ev = take_events();
+  if (!x || !qweight || !scales || !zeros || !y || !residual_in || !residual_out)
+    return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
+  laq_status st = check_shape(fn, N, K);
+  if (st != LAQ_OK) return st;
+  if (!laq::residual_linear_fits(N, K))
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "need K >= 2048 and rows whose activation tile fits in LDS (K <= ~28000)");
+  if (residual_out != residual_in && residual_out < residual_in + N && residual_in < residual_out + N)
+    return fail(LAQ_ERR_BAD_SHAPE, fn, "residual_out must equal residual_in or not overlap it");
+  if (!aligned(x, 16) || !aligned(qweight, 16)) return fail(LAQ_ERR_MISALIGNED, fn, "x and qweight must be 16-byte aligned");
+  if (!aligned(scales, 2) || !aligned(y, 2)) return fail(LAQ_ERR_MISALIGNED, fn, "scales and y must be 2-byte aligned");
+  if (!aligned(residual_in, 4) || !aligned(residual_out, 4))
+    return fail(LAQ_ERR_MISALIGNED, fn, "residual_in and residual_out must be 4-byte aligned");
+  return hip_status(fn, laq::launch_linear_residual<BITS>(
+                            static_cast<const uint16_t*>(x), qweight, static_cast<const uint16_t*>(scales), zeros,
+                            static_cast<uint16_t*>(y), residual_in, residual_out, N, K,
+                            static_cast<hipStream_t>(stream), ev));
+}
+
+template <int BITS>
 laq_status norm_mlp(const char* fn, const float* residual, const void* delta, const void* norm_weight, float eps,
                     float* residual_out, const uint32_t* gu_qweight, const void* gu_scales, const uint8_t* gu_zeros,
                     const uint32_t* down_qweight, const void* down_scales, const uint8_t* down_zeros, void* y,
@@ -437,6 +460,20 @@ laq_status norm_mlp(const char* fn, const float* residual, const void* delta, co
 }  // namespace
 
 extern "C" {
+
+laq_status laq_linear_residual_w3g128(const void* x, const uint32_t* qweight, const void* scales,
+                                      const uint8_t* zeros, void* y, const float* residual_in, float* residual_out,
+                                      int64_t N, int64_t K, void* stream) {
+  return linear_residual<3>("laq_linear_residual_w3g128", x, qweight, scales, zeros, y, residual_in, residual_out, N,
+                            K, stream);
+}
+
+laq_status laq_linear_residual_w4g128(const void* x, const uint32_t* qweight, const void* scales,
+                                      const uint8_t* zeros, void* y, const float* residual_in, float* residual_out,
+                                      int64_t N, int64_t K, void* stream) {
+  return linear_residual<4>("laq_linear_residual_w4g128", x, qweight, scales, zeros, y, residual_in, residual_out, N,
+                            K, stream);
+}
 
 int64_t laq_mlp_workspace_bytes(int64_t D, int64_t I) {
   const laq::MlpPlan p = laq::mlp_plan(D, I, 3);

@@ -91,6 +91,13 @@ struct LinearGroup {
   int waves;   // matrix-core group: waves per block
 };
 
+// Residual output stage of a batch-1 linear: res_out[n] = res_in[n] + y[n]
+// (fp32 plus the fp16 output) for every output row n.
+struct ResidualEpilogue {
+  const float* res_in = nullptr;
+  float* res_out = nullptr;
+};
+
 // Launchers (return the HIP error of the launch; shapes already validated).
 template <int BITS>
 hipError_t launch_quantize(const uint16_t* w, int64_t N, int64_t K, uint32_t* qweight,
@@ -138,6 +145,15 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
                          hipStream_t stream, const LaunchEvents& ev, float* workspace = nullptr,
                          size_t workspace_bytes = 0);
 
+// Configuration of the flat (VALU) kernel for MT = 1, 2 or 4 activation
+// rows (linear.hip): threads per block, staging loads per thread, rows per
+// block and per lane, LDS bytes.
+struct FlatPlan {
+  int NT = 256, XB = 2, R = 1, RPL = 1;
+  size_t lds = 0;
+};
+FlatPlan flat_plan(int MT, int64_t N, int G);
+
 // Gate|up linear with SiLU-and-multiply in its output stage: weight rows in
 // (gate, up) pairs, y fp16 [M][N/2].  Shapes: swiglu_fits(M, K), N even.
 bool swiglu_fits(int M, int64_t K);
@@ -173,6 +189,14 @@ template <int BITS>
 hipError_t launch_mlp(const NormPrologue& np, const uint32_t* gu_qw, const uint16_t* gu_s, const uint8_t* gu_z,
                       const uint32_t* dn_qw, const uint16_t* dn_s, const uint8_t* dn_z, uint16_t* y, int64_t D,
                       int64_t I, void* workspace, hipStream_t stream, const LaunchEvents& ev);
+
+// Batch-1 linear with the residual output stage (y = x w_hat^T, res_out =
+// res_in + y).  Shapes: residual_linear_fits(N, K).
+bool residual_linear_fits(int64_t N, int64_t K);
+template <int BITS>
+hipError_t launch_linear_residual(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
+                                  const uint8_t* zeros, uint16_t* y, const float* res_in, float* res_out, int64_t N,
+                                  int64_t K, hipStream_t stream, const LaunchEvents& ev);
 
 // Decode-step operations (decode.hip); head dimension 128.
 int64_t decode_attention_tiles(int64_t L);

@@ -440,11 +440,11 @@ __device__ __forceinline__ void pin_sgpr(T& v) {
 // Thread t takes units t + i*NT (i < UPT) of each pass over the block's
 // units; every launch uses UPT = 1 (more units per thread measured slower).
 // SW: the fused gate|up + SiLU-and-multiply output stage (swiglu_rows).
-template <int BITS, int MT, int NT, int UPT, int XB, bool SW = false, bool NORM = false>
+template <int BITS, int MT, int NT, int UPT, int XB, bool SW = false, bool NORM = false, bool RES = false>
 __device__ __forceinline__ void flat_block(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int block, const NormPrologue& np = NormPrologue{}) {
+    int block, const NormPrologue& np = NormPrologue{}, const ResidualEpilogue& re = ResidualEpilogue{}) {
   extern __shared__ u32x4 lds[];
   u32x4* xl = lds;                                                                // [MT][G][17]
   float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
@@ -511,6 +511,16 @@ __device__ __forceinline__ void flat_block(
   if constexpr (NORM) {
     pin_sgpr(npl.eps);
     pin_sgpr(npl.res_out);
+  }
+  // RES: the residual of row t / 16, read now by the lane that will write
+  // that row's output (every launch has rows <= NT / 16: one row per group
+  // of 16 lanes); rows past the block's read zero.
+  float rres = 0.0f;
+  float* res_out = re.res_out;
+  if constexpr (RES) {
+    pin_sgpr(res_out);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(re.res_in + row0, (uint32_t)rows * 4);
+    rres = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (uint32_t)(t >> 4) * 4, 0, 0));
   }
 
   // 3. Stage activations and per-group sums (first pass from the loads above).
@@ -598,7 +608,11 @@ __device__ __forceinline__ void flat_block(
         float acc = 0.0f;
         for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
         acc = row16_sum(acc);
-        if (l == 0 && m < M) yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+        if (l == 0 && m < M) {
+          const _Float16 yh = (_Float16)acc;
+          yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, yh);
+          if constexpr (RES) res_out[row0 + rr] = rres + (float)yh;
+        }
       }
     }
   }
@@ -608,11 +622,11 @@ __device__ __forceinline__ void flat_block(
 // form RPL layers of R1 = R / RPL rows (R1 * G <= NT), and thread
 // t = r*G + g of the first layer takes group g of rows r, r + R1, r + 2*R1,
 // ...  Loads, staging and the row sums are those of flat_block.
-template <int BITS, int MT, int NT, int RPL, int XB, bool SW = false, bool NORM = false>
+template <int BITS, int MT, int NT, int RPL, int XB, bool SW = false, bool NORM = false, bool RES = false>
 __device__ __forceinline__ void flat_block_rpl(
     const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
     const uint8_t* __restrict__ zeros, uint16_t* __restrict__ y, int M, int N, int G, int R, float inv_g,
-    int block, const NormPrologue& np = NormPrologue{}) {
+    int block, const NormPrologue& np = NormPrologue{}, const ResidualEpilogue& re = ResidualEpilogue{}) {
   extern __shared__ u32x4 lds[];
   u32x4* xl = lds;                                                                // [MT][G][17]
   float* xsum = reinterpret_cast<float*>(lds + (size_t)MT * G * kGroupStrideU4);  // [MT][G]
@@ -668,6 +682,16 @@ __device__ __forceinline__ void flat_block_rpl(
     pin_sgpr(npl.eps);
     pin_sgpr(npl.res_out);
   }
+  // RES: the residual of row t / 16, read now by the lane that will write
+  // that row's output (every launch has rows <= NT / 16: one row per group
+  // of 16 lanes); rows past the block's read zero.
+  float rres = 0.0f;
+  float* res_out = re.res_out;
+  if constexpr (RES) {
+    pin_sgpr(res_out);
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(re.res_in + row0, (uint32_t)rows * 4);
+    rres = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, (uint32_t)(t >> 4) * 4, 0, 0));
+  }
 
   // 2. Stage activations and per-group sums (first pass from the loads above).
   if constexpr (NORM) norm_finish<XB, NT>(nl_, npl, 128 * G, t, block == 0, xv);
@@ -706,7 +730,11 @@ __device__ __forceinline__ void flat_block_rpl(
         float acc = 0.0f;
         for (int g = l; g < G; g += 16) acc += part[m * R * G + rr * G + g];
         acc = row16_sum(acc);
-        if (l == 0 && m < M) yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, (_Float16)acc);
+        if (l == 0 && m < M) {
+          const _Float16 yh = (_Float16)acc;
+          yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, yh);
+          if constexpr (RES) res_out[row0 + rr] = rres + (float)yh;
+        }
       }
     }
   }
@@ -726,6 +754,29 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
     flat_block<BITS, MT, NT, 1, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(nblocks));
   else
     flat_block_rpl<BITS, MT, NT, RPL, XB, SW>(x, qw, scales, zeros, y, M, N, G, R, inv_g, xcd_block(nblocks));
+}
+
+// Batch-1 linear with the residual output stage: y = x w_hat^T as
+// linear_flat_kernel computes it, and res_out[n] = res_in[n] + y[n].  The
+// first fourteen dwords of arguments (preloaded) are what a wave needs before
+// its first requests, res_in included; fl(1/G) comes from v_rcp_f32, whose
+// error (one ulp) leaves trunc((t + 0.5) / G) exact for t < 1024 as in
+// flat_block.
+template <int BITS, int NT, int RPL, int XB>
+__global__ __launch_bounds__(NT) void linear_flat_res_kernel(
+    const uint16_t* __restrict__ x, const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales,
+    const uint8_t* __restrict__ zeros, int N, int G, int R, int nblocks, const float* __restrict__ res_in,
+    uint16_t* __restrict__ y, float* __restrict__ res_out) {
+  const float inv_g = __builtin_amdgcn_rcpf((float)G);
+  ResidualEpilogue re;
+  re.res_in = res_in;
+  re.res_out = res_out;
+  if constexpr (RPL == 1)
+    flat_block<BITS, 1, NT, 1, XB, false, false, true>(x, qw, scales, zeros, y, 1, N, G, R, inv_g,
+                                                       xcd_block(nblocks), NormPrologue{}, re);
+  else
+    flat_block_rpl<BITS, 1, NT, RPL, XB, false, false, true>(x, qw, scales, zeros, y, 1, N, G, R, inv_g,
+                                                             xcd_block(nblocks), NormPrologue{}, re);
 }
 
 // The same with the residual add + RMSNorm prologue (M = 1; no activation
@@ -1034,6 +1085,58 @@ int ceil_pow2(int v) {
 
 }  // namespace
 
+// Flat-unit kernel configuration for MT activation rows (1, 2, 4) and rows
+// of G groups: one (row, group) unit per thread (fewest loads per lane
+// measured best on every shape) and whole rows per block, so the reduction
+// stays inside the block.  The caller uses it when lds fits the 64 KB budget.
+//  - Threads per block: every block stages the whole activation row, so
+//    longer rows want more rows per block (about 8 or more) to amortize it;
+//    short rows with few of them use smaller blocks so that the grid still
+//    covers the compute units.  Rows of 65..128 groups use 256 threads at one
+//    activation row and 512 at two, with two rows per lane (below).
+//  - Rows per lane: a thread takes group g of RPL rows, so every activation
+//    group read from LDS serves RPL rows and each block's activation tile
+//    serves RPL times as many rows; the lane's dot products get RPL times
+//    longer.  Measured on MI355X, two rows per lane pay off when
+//     - one activation row has 65..128 groups,
+//     - the grid at one row per lane holds more waves than the chip keeps
+//       resident (32 per compute unit), so waves would run in several rounds,
+//     - two activation rows meet rows of 32..128 groups (twice the LDS
+//       reads per unit);
+//    elsewhere one row per lane is faster (the lanes' own latency decides).
+FlatPlan flat_plan(int MT, int64_t N, int G) {
+  FlatPlan p;
+  int NT = G <= 32 ? 256 : G <= 64 ? 512 : G <= 128 ? (MT == 1 ? 256 : 512) : 1024;
+  if (MT == 1)
+    while (NT > 64 && G <= 16 && NT / 2 >= G && (N + NT / G - 1) / (NT / G) < 256) NT /= 2;
+  const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
+  auto lds_bytes = [&](int rows) { return (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * rows * G * 4; };
+  int R = max(1, NT / G);
+  R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
+  int want;
+  {
+    const int64_t waves1 = (N + R - 1) / R * (NT / 64);
+    if (MT == 1)
+      want = (G > 64 && G <= 128) || (G <= 64 && waves1 > kResidentWaves) ? 2 : 1;
+    else
+      want = (MT == 2 && G >= 32 && G <= 128) ? 2 : 1;
+  }
+  int RPL = 1;
+  if (want > 1 && NT >= 256 && G <= NT) {
+    const int r1 = min(NT / G, 4096 / (G * MT * want));
+    if (r1 >= 1 && lds_bytes(want * r1) <= 64 * 1024) {
+      RPL = want;
+      R = want * r1;
+    }
+  }
+  p.NT = NT;
+  p.XB = XB;
+  p.R = R;
+  p.RPL = RPL;
+  p.lds = lds_bytes(R);
+  return p;
+}
+
 template <int BITS>
 hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
                          const uint8_t* zeros, uint16_t* y, int M, int64_t N, int64_t K,
@@ -1047,50 +1150,9 @@ hipError_t launch_linear(const uint16_t* x, const uint32_t* qweight, const uint1
   const u32x4* x4 = reinterpret_cast<const u32x4*>(x);
   const u32x4* q4 = reinterpret_cast<const u32x4*>(qweight);
   {
-    // Flat-unit kernel when the activation tile and the partials fit in LDS.
-    // One (row, group) unit per thread (fewest loads per lane measured best on
-    // every shape) and whole rows per block, so the reduction stays inside
-    // the block.
-    // Threads per block: every block stages the whole activation row, so
-    // longer rows want more rows per block (about 8 or more) to amortize it;
-    // short rows with few of them use smaller blocks so that the grid still
-    // covers the compute units.
-    // Rows of 65..128 groups use 256 threads at one activation row and 512
-    // at two, with two rows per lane (below).
-    int NT = G <= 32 ? 256 : G <= 64 ? 512 : G <= 128 ? (MT == 1 ? 256 : 512) : 1024;
-    if (MT == 1)
-      while (NT > 64 && G <= 16 && NT / 2 >= G && (N + NT / G - 1) / (NT / G) < 256) NT /= 2;
-    const int XB = (MT * G * 16 <= 2 * NT) ? 2 : 5;
-    auto lds_bytes = [&](int rows) { return (size_t)MT * G * (kGroupStrideU4 * 16 + 4) + (size_t)MT * rows * G * 4; };
-    int R = max(1, NT / G);
-    R = max(1, min(R, 4096 / (G * MT)));  // partials: at most 16 KB
-    // Rows per lane: a thread takes group g of RPL rows, so every activation
-    // group read from LDS serves RPL rows and each block's activation tile
-    // serves RPL times as many rows; the lane's dot products get RPL times
-    // longer.  Measured on MI355X, two rows per lane pay off when
-    //  - one activation row has 65..128 groups,
-    //  - the grid at one row per lane holds more waves than the chip keeps
-    //    resident (32 per compute unit), so waves would run in several rounds,
-    //  - two activation rows meet rows of 32..128 groups (twice the LDS
-    //    reads per unit);
-    // elsewhere one row per lane is faster (the lanes' own latency decides).
-    int want;
-    {
-      const int64_t waves1 = (N + R - 1) / R * (NT / 64);
-      if (MT == 1)
-        want = (G > 64 && G <= 128) || (G <= 64 && waves1 > kResidentWaves) ? 2 : 1;
-      else
-        want = (MT == 2 && G >= 32 && G <= 128) ? 2 : 1;
-    }
-    int RPL = 1;
-    if (want > 1 && NT >= 256 && G <= NT) {
-      const int r1 = min(NT / G, 4096 / (G * MT * want));
-      if (r1 >= 1 && lds_bytes(want * r1) <= 64 * 1024) {
-        RPL = want;
-        R = want * r1;
-      }
-    }
-    const size_t lds = lds_bytes(R);
+    const FlatPlan fp = flat_plan(MT, N, G);
+    const int NT = fp.NT, XB = fp.XB, R = fp.R, RPL = fp.RPL;
+    const size_t lds = fp.lds;
     if (MT <= 4 && lds <= 64 * 1024) {
       const int nblocks = (int)((N + R - 1) / R);
       const unsigned blocks = xcd_grid(nblocks);
@@ -1245,6 +1307,43 @@ hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, c
   return hipGetLastError();
 }
 
+bool residual_linear_fits(int64_t N, int64_t K) {
+  // At least 16 groups: a block's rows then fit one row per 16 lanes.
+  if (N < 1 || K < 2048 || K % 128 != 0) return false;
+  const FlatPlan fp = flat_plan(1, N, (int)(K / 128));
+  return fp.lds <= 64 * 1024 && fp.R <= fp.NT / 16;
+}
+
+template <int BITS>
+hipError_t launch_linear_residual(const uint16_t* x, const uint32_t* qweight, const uint16_t* scales,
+                                  const uint8_t* zeros, uint16_t* y, const float* res_in, float* res_out, int64_t N,
+                                  int64_t K, hipStream_t stream, const LaunchEvents& ev) {
+  // The M = 1 flat kernel's configuration, so y is the plain call's, bit for bit.
+  if (!residual_linear_fits(N, K)) return hipErrorInvalidValue;
+  const int G = (int)(K / 128);
+  const FlatPlan fp = flat_plan(1, N, G);
+  const int nblocks = (int)((N + fp.R - 1) / fp.R);
+  const dim3 grid(xcd_grid(nblocks));
+#define LAQ_RES_K(NTV, RPLV, XBV)                                                                                 \
+  launch(linear_flat_res_kernel<BITS, NTV, RPLV, XBV>, grid, dim3(NTV), (uint32_t)fp.lds, stream, ev, x, qweight, \
+         scales, zeros, (int)N, G, fp.R, nblocks, res_in, y, res_out)
+#define LAQ_RES_RPL(NTV, XBV)                   \
+  do {                                          \
+    if (fp.RPL == 2) LAQ_RES_K(NTV, 2, XBV);    \
+    else LAQ_RES_K(NTV, 1, XBV);                \
+  } while (0)
+  if (fp.NT == 256 && fp.XB == 2) LAQ_RES_RPL(256, 2);
+  else if (fp.NT == 256) LAQ_RES_RPL(256, 5);
+  else if (fp.NT == 512) LAQ_RES_RPL(512, 2);
+  else if (fp.NT == 1024) LAQ_RES_RPL(1024, 5);
+  else if (fp.NT == 128) LAQ_RES_K(128, 1, 2);
+  else if (fp.NT == 64) LAQ_RES_K(64, 1, 2);
+  else return hipErrorInvalidValue;
+#undef LAQ_RES_RPL
+#undef LAQ_RES_K
+  return hipGetLastError();
+}
+
 MlpPlan mlp_plan(int64_t D, int64_t I, int bits) {
   MlpPlan p;
   if (D < 128 || D % 128 != 0 || D > kMlpMaxHidden || I < 128 || I % 128 != 0 || I > kMlpMaxInter) return p;
@@ -1374,6 +1473,12 @@ template hipError_t launch_linear_norm<3>(const NormPrologue&, const uint32_t*, 
                                           uint16_t*, int64_t, int64_t, bool, hipStream_t, const LaunchEvents&);
 template hipError_t launch_linear_norm<4>(const NormPrologue&, const uint32_t*, const uint16_t*, const uint8_t*,
                                           uint16_t*, int64_t, int64_t, bool, hipStream_t, const LaunchEvents&);
+template hipError_t launch_linear_residual<3>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
+                                              uint16_t*, const float*, float*, int64_t, int64_t, hipStream_t,
+                                              const LaunchEvents&);
+template hipError_t launch_linear_residual<4>(const uint16_t*, const uint32_t*, const uint16_t*, const uint8_t*,
+                                              uint16_t*, const float*, float*, int64_t, int64_t, hipStream_t,
+                                              const LaunchEvents&);
 template hipError_t launch_mlp<3>(const NormPrologue&, const uint32_t*, const uint16_t*, const uint8_t*,
                                   const uint32_t*, const uint16_t*, const uint8_t*, uint16_t*, int64_t, int64_t,
                                   void*, hipStream_t, const LaunchEvents&);

@@ -58,6 +58,10 @@ class DecodeStep:
     receiving the down projection's output, fp16 [1][hidden]) is the whole MLP
     block after the attention: norm, gate|up, SiLU-and-multiply and down
     (laq.add_rmsnorm_mlp, one kernel); the step then skips the down call.
+    An o or down callable with an attribute residual_linear = g(x,
+    residual_in, residual_out, out) adds its output to the residual stream
+    itself (laq.linear_residual: residual_out = residual_in + out); the next
+    norm then runs with no delta.
     """
 
     def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None,
@@ -105,6 +109,17 @@ class DecodeStep:
         laq.add_rmsnorm(self._res[self._cur], delta, weight, self.s["eps"], out=self.h)
         f(self.h, out)
 
+    def _linear(self, f, x, out):
+        """f(x, out); returns the delta the next norm adds: out, or None when
+        f added it to the residual stream itself."""
+        g = getattr(f, "residual_linear", None)
+        if g is None:
+            f(x, out)
+            return out
+        g(x, self._res[self._cur], self._res[1 - self._cur], out)
+        self._cur = 1 - self._cur
+        return None
+
     def run(self, pos):
         """Decode the token at position pos (attends to positions 0..pos).
         Returns the logits when the step has an LM head, else the final
@@ -125,20 +140,19 @@ class DecodeStep:
                                  self.v_caches[l], q_out=self.q)
                 laq.decode_attention(self.q, self.k_caches[l], self.v_caches[l], pos + 1, out=self.attn,
                                      workspace=self.workspace)
-            f_o(self.attn.view(1, Hq * HEAD_DIM), self.o)
+            delta = self._linear(f_o, self.attn.view(1, Hq * HEAD_DIM), self.o)
             mlp = getattr(f_gu, "norm_mlp", None)
             if mlp is not None:
-                mlp(self._res[self._cur], self.o, w_post, eps, self._res[1 - self._cur], self.down)
+                mlp(self._res[self._cur], delta, w_post, eps, self._res[1 - self._cur], self.down)
                 self._cur = 1 - self._cur
                 delta = self.down
                 continue
             if getattr(f_gu, "swiglu", False):
-                self._norm(f_gu, self.o, w_post, self.m)
+                self._norm(f_gu, delta, w_post, self.m)
             else:
-                self._norm(f_gu, self.o, w_post, self.gu)
+                self._norm(f_gu, delta, w_post, self.gu)
                 laq.silu_mul(self.gu, out=self.m)
-            f_down(self.m, self.down)
-            delta = self.down
+            delta = self._linear(f_down, self.m, self.down)
         if self.lm_head is not None and getattr(self.lm_head, "norm_linear", None) is not None:
             self._norm(self.lm_head, delta, self.final_norm, self.logits)
             return self.logits

@@ -32,7 +32,8 @@ EXPORTS = ("laq_abi_version", "laq_status_string", "laq_last_error", "laq_profil
            "laq_linear_swiglu_w4g128", "laq_linear_noalloc_w3g128", "laq_decode_attention_qkv_workspace_bytes",
            "laq_decode_attention_qkv_f16", "laq_add_rmsnorm_linear_w3g128", "laq_add_rmsnorm_linear_w4g128",
            "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128",
-           "laq_mlp_workspace_bytes", "laq_add_rmsnorm_mlp_w3g128")
+           "laq_mlp_workspace_bytes", "laq_add_rmsnorm_mlp_w3g128", "laq_linear_residual_w3g128",
+           "laq_linear_residual_w4g128")
 HEAD_DIM = 128
 
 
@@ -107,9 +108,14 @@ def lib():
         L.laq_silu_mul_f16.restype = ctypes.c_int32
         for name in ("laq_add_rmsnorm_linear_w3g128", "laq_add_rmsnorm_linear_w4g128",
                      "laq_add_rmsnorm_linear_swiglu_w3g128", "laq_add_rmsnorm_linear_swiglu_w4g128",
-           "laq_mlp_workspace_bytes", "laq_add_rmsnorm_mlp_w3g128"):
+           "laq_mlp_workspace_bytes", "laq_add_rmsnorm_mlp_w3g128", "laq_linear_residual_w3g128",
+           "laq_linear_residual_w4g128"):
             f = getattr(L, name)
             f.argtypes = [P, P, P, F32, P, P, P, P, P, I64, I64, P]
+            f.restype = ctypes.c_int32
+        for name in ("laq_linear_residual_w3g128", "laq_linear_residual_w4g128"):
+            f = getattr(L, name)
+            f.argtypes = [P, P, P, P, P, P, P, I64, I64, P]
             f.restype = ctypes.c_int32
         L.laq_mlp_workspace_bytes.argtypes = [I64, I64]
         L.laq_mlp_workspace_bytes.restype = I64
@@ -226,6 +232,26 @@ def linear_noalloc_w3g128(x, qweight, scales, zeros, out=None):
     y = torch.empty((M, N), dtype=torch.float16, device=x.device) if out is None else out
     _check(lib().laq_linear_noalloc_w3g128(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N, K,
                                            _stream(x.device)))
+    return y
+
+
+def linear_residual(x, qweight, scales, zeros, residual_in, residual_out, bits=3, out=None):
+    """One token's linear that also updates the residual stream: y = x @
+    w_hat^T (fp16 [1][N], as `linear` computes it) and residual_out =
+    residual_in + y (fp32 [1][N]; may be residual_in itself)."""
+    import torch
+    assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.shape[0] == 1 and x.is_contiguous()
+    K = x.shape[1]
+    N = scales.shape[0]
+    assert qweight.numel() == packed_words(bits, N, K) and qweight.is_contiguous()
+    assert scales.shape == (N, K // GROUP) and zeros.shape == (N, K // GROUP)
+    assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
+    for r in (residual_in, residual_out):
+        assert r.dtype == torch.float32 and r.numel() == N and r.is_contiguous()
+    y = torch.empty((1, N), dtype=torch.float16, device=x.device) if out is None else out
+    fn = lib().laq_linear_residual_w3g128 if bits == 3 else lib().laq_linear_residual_w4g128
+    _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), _ptr(residual_in), _ptr(residual_out), N,
+              K, _stream(x.device)))
     return y
 
 

@@ -142,6 +142,26 @@ def test_add_rmsnorm_linear_validation(L, bits, swiglu):
     assert b"laq_add_rmsnorm_linear" in L.laq_last_error()
 
 
+def _lres(L, bits, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, ri=FAKE, ro=FAKE + 0x10000, N=2560, K=4096):
+    f = L.laq_linear_residual_w3g128 if bits == 3 else L.laq_linear_residual_w4g128
+    return f(ctypes.c_void_p(x), ctypes.c_void_p(q), ctypes.c_void_p(s), ctypes.c_void_p(z), ctypes.c_void_p(y),
+             ctypes.c_void_p(ri), ctypes.c_void_p(ro), N, K, None)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_linear_residual_validation(L, bits):
+    for kw in ("x", "q", "s", "z", "y", "ri", "ro"):
+        assert _lres(L, bits, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _lres(L, bits, N=0) == laq.LAQ_ERR_BAD_SHAPE
+    assert _lres(L, bits, K=1920) == laq.LAQ_ERR_BAD_SHAPE          # fewer than 16 groups
+    assert _lres(L, bits, K=32768) == laq.LAQ_ERR_BAD_SHAPE         # activation tile past the LDS budget
+    assert _lres(L, bits, ro=FAKE + 4 * 100) == laq.LAQ_ERR_BAD_SHAPE  # partial overlap
+    assert _lres(L, bits, x=FAKE + 8) == laq.LAQ_ERR_MISALIGNED
+    assert _lres(L, bits, s=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
+    assert _lres(L, bits, ri=FAKE + 2) == laq.LAQ_ERR_MISALIGNED
+    assert b"laq_linear_residual" in L.laq_last_error()
+
+
 def _mlp(L, r=FAKE, d=FAKE, w=FAKE, eps=1e-6, ro=FAKE + 0x10000, gq=FAKE, gs=FAKE, gz=FAKE, dq=FAKE, ds=FAKE,
          dz=FAKE, y=FAKE, D=256, I=384, ws=FAKE, ws_bytes=1 << 20):
     return L.laq_add_rmsnorm_mlp_w3g128(

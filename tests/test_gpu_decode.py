@@ -206,6 +206,41 @@ def test_add_rmsnorm_linear(bits, swiglu, N, K, with_delta):
     assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
 
 
+RESIDUAL_CASES = [(3, 2560, 4096), (3, 2560, 9728), (4, 2560, 4096), (3, 4100, 2048), (3, 1000, 8192),
+                  (4, 517, 9728), (3, 33, 2560)]
+
+
+@pytest.mark.parametrize("bits,N,K", RESIDUAL_CASES)
+def test_linear_residual(bits, N, K):
+    """laq_linear_residual (a batch-1 linear that also writes residual_in + y
+    to the residual stream): y against the oracle's linear within the linear
+    tolerance and bit for bit equal to the plain laq_linear call; the new
+    residual bitwise equal to residual_in + y in fp32; in place as well.
+    Qwen3-4B's o (2560 x 4096) and down (2560 x 9728, two rows per lane), a
+    ragged 4100 x 2048, 1000 x 8192, W4, 33 rows."""
+    say("linear_residual", bits, N, K)
+    rng = np.random.default_rng(N + K + bits)
+    x = inputs.activations(1, K, cfg=47, layer=bits)
+    w = inputs.weights(N, K, cfg=47, layer=bits, proj=K % 89)
+    codes, sc, z = oracle.quantize(w, bits)
+    q, sd, zd = dev(oracle.pack(codes, bits).view(np.int32)), dev(sc.view(np.float16)), dev(z)
+    res = (rng.standard_normal((1, N)) * 3).astype(np.float32)
+    rd = dev(res)
+    ro = torch.full((1, N), float("nan"), dtype=torch.float32, device=DEV)
+    y = laq.linear_residual(dev(x), q, sd, zd, rd, ro, bits)
+    y_plain = laq.linear(dev(x), q, sd, zd, bits)
+    torch.cuda.synchronize()
+    r = linear_check(y.cpu().numpy(), oracle.linear(x, codes, sc, z))
+    assert r["ok"], r
+    assert torch.equal(y.view(torch.int16), y_plain.view(torch.int16))
+    expect = res + y.cpu().numpy().astype(np.float32)
+    assert np.array_equal(ro.cpu().numpy(), expect)
+    assert np.array_equal(rd.cpu().numpy(), res)
+    laq.linear_residual(dev(x), q, sd, zd, rd, rd, bits)  # in place
+    torch.cuda.synchronize()
+    assert np.array_equal(rd.cpu().numpy(), expect)
+
+
 MLP_CASES = [(2560, 9728, True), (256, 384, True), (1024, 128, False), (1280, 128 * 77, True), (2560, 1152, False)]
 
 
@@ -612,6 +647,127 @@ def test_decode_step_fused_norms_vs_oracle(merged_mlp):
     assert np.array_equal(step.residual.cpu().numpy(), e_lm["res_out"])
 
     # HIP graph of the same step (recording wrappers copy tensors, which the graph captures too)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        step.run(pos)
+    for _ in range(3):
+        step.logits.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(step.logits.view(torch.int16), logits.view(torch.int16))
+        step.run(pos)
+        torch.cuda.synchronize()
+        assert torch.equal(step.logits.view(torch.int16), logits.view(torch.int16))
+
+
+def test_decode_step_residual_producers_vs_oracle():
+    """DecodeStep with the norms inside q|k|v, gate|up (SiLU output stage) and
+    the LM head, and with o and down adding their outputs to the residual
+    stream themselves (laq.linear_residual), so that every norm runs with no
+    delta: two Qwen3-4B-shaped layers plus an LM head (4096 rows), W3 on
+    oracle-quantized codes, at position 200 of a filled cache.  Each
+    producer's output matches the oracle's linear on its own input and its new
+    residual equals its input residual plus that output (fp32, bit for bit);
+    each norm's residual is the last producer's (the token's embedding first)
+    and its linear matches the oracle's linear on the oracle's RMSNorm of it;
+    attention matches the oracle; three replays of a HIP-graph capture give
+    the eager logits bit for bit."""
+    say("decode step with residual producers vs oracle")
+    from paper_2605_08755_amd import decode
+    shape = dict(decode.QWEN3_4B, layers=2, vocab=4096)
+    D, Hq, Hkv, I, S, V, pos = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256, 4096, 200
+    rng = np.random.default_rng(31)
+    rec = []
+
+    def norm_lin(kind, l, q, s, z, swiglu):
+        def f(x, out):  # unused by the step (norm_linear is present)
+            laq.linear(x, q, s, z, 3, out=out)
+
+        def g(res, delta, w, eps, res_out, out):
+            laq.add_rmsnorm_linear(res, delta, w, eps, q, s, z, 3, swiglu=swiglu, out=out, residual_out=res_out)
+            rec.append({"kind": kind, "layer": l, "res": res.clone(), "delta": None if delta is None else delta.clone(),
+                        "res_out": res_out.clone(), "out": out.clone()})
+        f.norm_linear = g
+        f.swiglu = swiglu
+        return f
+
+    def producer(kind, l, q, s, z):
+        def f(x, out):  # unused by the step (residual_linear is present)
+            laq.linear(x, q, s, z, 3, out=out)
+
+        def g(x, r_in, r_out, out):
+            laq.linear_residual(x, q, s, z, r_in, r_out, 3, out=out)
+            rec.append({"kind": kind, "layer": l, "x": x.clone(), "res_in": r_in.clone(), "res_out": r_out.clone(),
+                        "out": out.clone()})
+        f.residual_linear = g
+        return f
+
+    host, lins = [], []
+    for l in range(2):
+        hl, fl = {}, []
+        for j, (name, N, K) in enumerate((("qkv", (Hq + 2 * Hkv) * 128, D), ("o", D, Hq * 128),
+                                          ("gu", 2 * I, D), ("down", D, I))):
+            hq, (q, s, z) = _quantized(N, K, 48, l, j, interleave_halves=name == "gu")
+            hl[name] = hq
+            fl.append(norm_lin(name, l, q, s, z, name == "gu") if name in ("qkv", "gu") else producer(name, l, q, s, z))
+        host.append(hl)
+        lins.append(fl)
+    h_lm, (q_lm, s_lm, z_lm) = _quantized(V, D, 48, 9, 0)
+    norms_h = [tuple((1 + 0.1 * rng.standard_normal(n)).astype(np.float16) for n in (D, D, 128, 128))
+               for _ in range(2)]
+    fin_h = (1 + 0.1 * rng.standard_normal(D)).astype(np.float16)
+    kc_h = [f16(rng, (Hkv, S, 128)) for _ in range(2)]
+    vc_h = [f16(rng, (Hkv, S, 128)) for _ in range(2)]
+    x0_h = rng.standard_normal((1, D)).astype(np.float32)
+    norms = [tuple(dev(a) for a in nl) for nl in norms_h]
+    kcs, vcs = [dev(a) for a in kc_h], [dev(a) for a in vc_h]
+    step = decode.DecodeStep(shape, [tuple(f) for f in lins], norms, dev(fin_h), kcs, vcs, DEV,
+                             lm_head=norm_lin("lm", 2, q_lm, s_lm, z_lm, False))
+    step.x0.copy_(dev(x0_h))
+    logits = step.run(pos).clone()
+    torch.cuda.synchronize()
+    g = {(e["kind"], e["layer"]): {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in e.items()}
+         for e in rec}
+    assert len(g) == 9
+
+    def check(name, got, ref):
+        r = linear_check(got, ref)
+        assert r["ok"], (name, r)
+
+    def normed(e, w):
+        assert e["delta"] is None
+        assert np.array_equal(e["res_out"], e["res"])
+        return np.asarray(OD.rmsnorm(e["res"], w, EPS)).astype(np.float16)
+
+    def produced(e, hq):
+        check((e["kind"], e["layer"]), e["out"], oracle.linear(e["x"], *hq))
+        assert np.array_equal(e["res_out"], e["res_in"] + e["out"].astype(np.float32)), e["kind"]
+
+    res_prev = x0_h
+    for l in range(2):
+        w_in, w_post, qn, kn = norms_h[l]
+        e_qkv, e_o, e_gu, e_dn = (g[(k, l)] for k in ("qkv", "o", "gu", "down"))
+        assert np.array_equal(e_qkv["res"], res_prev)
+        check(("qkv", l), e_qkv["out"], oracle.linear(normed(e_qkv, w_in), *host[l]["qkv"]))
+        q_ref, k_ref, v_ref = OD.qk_norm_rope(e_qkv["out"], qn, kn, pos, Hq, Hkv, 128, EPS, THETA)
+        kc, vc = kcs[l].cpu().numpy(), vcs[l].cpu().numpy()
+        check(("k cache row", l), kc[:, pos], k_ref)
+        assert np.array_equal(vc[:, pos], v_ref.astype(np.float16))
+        check(("attention", l), e_o["x"].reshape(Hq, 128),
+              OD.decode_attention(q_ref.astype(np.float16), kc[:, :pos + 1], vc[:, :pos + 1]))
+        assert np.array_equal(e_o["res_in"], e_qkv["res_out"])
+        produced(e_o, host[l]["o"])
+        assert np.array_equal(e_gu["res"], e_o["res_out"])
+        full = np.asarray(oracle.linear(normed(e_gu, w_post), *host[l]["gu"]), dtype=np.float64)
+        check(("gate|up + silu", l), e_gu["out"], OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I))
+        assert np.array_equal(e_dn["x"], e_gu["out"]) and np.array_equal(e_dn["res_in"], e_gu["res_out"])
+        produced(e_dn, host[l]["down"])
+        res_prev = e_dn["res_out"]
+    e_lm = g[("lm", 2)]
+    assert np.array_equal(e_lm["res"], res_prev)
+    check("logits", logits.cpu().numpy(), oracle.linear(normed(e_lm, fin_h), *h_lm))
+
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
         step.run(pos)
