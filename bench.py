@@ -602,14 +602,39 @@ def summarize_trace(path, launches, steps):
     return "\n".join(lines)
 
 
+def kernel_table(path):
+    """Markdown table of every library kernel in a rocprofv3 kernel_trace.csv
+    (any run of this file): per kernel name and grid, dispatches, average,
+    median and minimum End - Start in µs, and the total in ms."""
+    import csv
+    by = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"]
+            if "laq::" not in name:
+                continue
+            name = name.replace("(anonymous namespace)::", "").replace("void ", "").replace("laq::", "")
+            key = (name.split("(")[0], r.get("Grid_Size_X", r.get("Grid_Size", "")),
+                   r.get("Workgroup_Size_X", r.get("Workgroup_Size", "")))
+            by.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    med = lambda v: sorted(v)[len(v) // 2]
+    lines = ["| kernel | grid | block | dispatches | avg µs | p50 µs | min µs | total ms |",
+             "|---|---|---|---|---|---|---|---|"]
+    for (k, g, b), v in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        lines.append("| %s | %s | %s | %d | %.3f | %.3f | %.3f | %.2f |"
+                     % (k, g, b, len(v), sum(v) / len(v), med(v), min(v), sum(v) / 1e3))
+    return "\n".join(lines)
+
+
 def pmc_summary(fetch_csv, write_csv, launches, steps):
     """Per-launch HBM bytes of the GEMV from two rocprofv3 --pmc runs of
     --profile-run (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each
     scaled by what the counter reads for the 256 MiB device copy that
-    --profile-run performs first."""
+    --profile-run performs first.  Also per library kernel and grid: the
+    dispatches and the mean raw counter values (KiB, unscaled)."""
     import csv
 
-    def load(path, counter):
+    def load(path, counter, per):
         copy, lin = [], []
         with open(path) as f:
             for r in csv.DictReader(f):
@@ -617,13 +642,17 @@ def pmc_summary(fetch_csv, write_csv, launches, steps):
                     continue
                 v = float(r["Counter_Value"])
                 name = r["Kernel_Name"]
+                if "laq::" in name:
+                    tail = name.replace("(anonymous namespace)::", "").replace("void ", "").replace("laq::", "")
+                    per.setdefault((tail.split("(")[0], r.get("Grid_Size", "")), {}).setdefault(counter, []).append(v)
                 if "linear" in name:
                     lin.append(v)
                 elif "copy" in name.lower() or "elementwise" in name.lower():
                     copy.append(v)
         return copy, lin
-    cf, lf = load(fetch_csv, "FETCH_SIZE")
-    cw, lw = load(write_csv, "WRITE_SIZE")
+    per = {}
+    cf, lf = load(fetch_csv, "FETCH_SIZE", per)
+    cw, lw = load(write_csv, "WRITE_SIZE", per)
     nbytes_kib = (256 << 20) / 1024
     fscale = nbytes_kib / max(cf)
     wscale = nbytes_kib / max(cw)
@@ -634,7 +663,14 @@ def pmc_summary(fetch_csv, write_csv, launches, steps):
             "calibration": "256 MiB device copy: FETCH_SIZE %.0f KiB, WRITE_SIZE %.0f KiB (read and written: "
                            "%.0f KiB each)" % (max(cf), max(cw), nbytes_kib),
             "fetch_bytes_per_launch": int(round(fetch)), "write_bytes_per_launch": int(round(write)),
-            "hbm_bytes_per_launch": int(round(fetch + write)), "dispatches": len(lf)}
+            "hbm_bytes_per_launch": int(round(fetch + write)), "dispatches": len(lf),
+            "per_kernel_raw_kib": [{"kernel": k, "grid": g,
+                                    "dispatches": len(c.get("FETCH_SIZE", [])),
+                                    "FETCH_SIZE": round(sum(c["FETCH_SIZE"]) / len(c["FETCH_SIZE"]), 1)
+                                    if c.get("FETCH_SIZE") else None,
+                                    "WRITE_SIZE": round(sum(c["WRITE_SIZE"]) / len(c["WRITE_SIZE"]), 1)
+                                    if c.get("WRITE_SIZE") else None}
+                                   for (k, g), c in sorted(per.items())]}
 
 
 def kernel_durations(stack, M, bits, reps):
@@ -764,6 +800,8 @@ def main():
                     help="for rocprofv3 --kernel-trace: the headline step's graph, --warmup + --steps replays only")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print a markdown summary of a --trace-run kernel trace (last --steps replays) and exit")
+    ap.add_argument("--kernel-table", metavar="KERNEL_TRACE_CSV",
+                    help="print per-kernel dispatch statistics of any kernel trace of this file and exit")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the per-launch HBM bytes of --profile-run counter collections and exit")
     ap.add_argument("--launches", type=int, default=144, help="GEMV launches per step (for the summaries)")
@@ -771,6 +809,9 @@ def main():
 
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace, args.launches, args.steps))
+        return
+    if args.kernel_table:
+        print(kernel_table(args.kernel_table))
         return
     if args.pmc_summary:
         rec = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.launches, args.steps)

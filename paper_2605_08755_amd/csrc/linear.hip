@@ -780,12 +780,12 @@ __global__ __launch_bounds__(NT) void linear_flat_res_kernel(
 }
 
 // The same with the residual add + RMSNorm prologue (M = 1; no activation
-// pointer: the row is formed from np).
+// pointer: the row is formed from np, XB units of 8 elements per thread).
 // The first fourteen dwords of arguments (preloaded in scalar registers) are
 // what a wave needs before its first requests: the three prologue rows, the
 // weights, N and the packed shape gr = G | R << 8 (G <= 64, R <= 512); the
 // block count and fl(1/G) are derived from them.
-template <int NT, int RPL, bool SW, int BITS>
+template <int NT, int RPL, bool SW, int BITS, int XB>
 __global__ __launch_bounds__(NT) void linear_flat_norm_kernel(
     const float* __restrict__ res_in, const uint16_t* __restrict__ delta, const uint16_t* __restrict__ weight,
     const uint32_t* __restrict__ qw, const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zeros, int N,
@@ -800,9 +800,9 @@ __global__ __launch_bounds__(NT) void linear_flat_norm_kernel(
   np.res_out = res_out;
   np.eps = eps;
   if constexpr (RPL == 1)
-    flat_block<BITS, 1, NT, 1, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(nblocks), np);
+    flat_block<BITS, 1, NT, 1, XB, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g, xcd_block(nblocks), np);
   else
-    flat_block_rpl<BITS, 1, NT, RPL, 2, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g,
+    flat_block_rpl<BITS, 1, NT, RPL, XB, SW, true>(nullptr, qw, scales, zeros, y, 1, N, G, R, inv_g,
                                                   xcd_block(nblocks), np);
 }
 
@@ -1268,14 +1268,19 @@ template <int BITS>
 hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, const uint16_t* scales,
                               const uint8_t* zeros, uint16_t* y, int64_t N, int64_t K, bool swiglu,
                               hipStream_t stream, const LaunchEvents& ev) {
-  // The M = 1 flat kernel's configuration (threads, rows per block, rows per
-  // lane as launch_linear chooses them), with blocks of 256 threads up to 32
-  // groups and 512 up to 64, so that two staging units per thread cover the
-  // row: the prologue needs the whole row in registers before its one
-  // reduction.
+  // The M = 1 flat kernel's configuration (rows per block, rows per lane as
+  // launch_linear chooses them).  The prologue needs the whole row in
+  // registers before its one reduction, XB units of 8 elements per thread:
+  // blocks of 256 threads up to 16 groups and 512 up to 64, so that one unit
+  // per thread covers rows up to 32 groups and two up to 64.  (Measured on
+  // MI355X, Qwen3-4B decode step: 512-thread blocks with one prologue unit
+  // per thread for the 20-group q|k|v and gate|up rows instead of 256 with
+  // two, 1005-1008 -> 996-997 us per token; the prologue's loads and its
+  // row reads are per block, so fewer, larger blocks issue fewer of them.)
   if (!norm_linear_fits(K) || (swiglu && N % 2 != 0)) return hipErrorInvalidValue;
   const int G = (int)(K / 128);
-  const int NT = G <= 32 ? 256 : 512;
+  const int NT = G <= 16 ? 256 : 512;
+  const bool one_unit = K <= 8 * NT;
   auto lds_bytes = [&](int rows) { return (size_t)G * (kGroupStrideU4 * 16 + 4) + (size_t)rows * G * 4; };
   int R = max(1, min(NT / G, 4096 / G));
   int RPL = 1;
@@ -1291,17 +1296,21 @@ hipError_t launch_linear_norm(const NormPrologue& np, const uint32_t* qweight, c
   const size_t lds = lds_bytes(R);
   const int nblocks = (int)((N + R - 1) / R);
   const dim3 grid(xcd_grid(nblocks));
-#define LAQ_NORM_K(NTV, RPLV, SWV)                                                                                \
-  launch(linear_flat_norm_kernel<NTV, RPLV, SWV, BITS>, grid, dim3(NTV), (uint32_t)lds, stream, ev, np.res_in,     \
+#define LAQ_NORM_K(NTV, RPLV, SWV, XBV)                                                                           \
+  launch(linear_flat_norm_kernel<NTV, RPLV, SWV, BITS, XBV>, grid, dim3(NTV), (uint32_t)lds, stream, ev, np.res_in, \
          np.delta, np.weight, qweight, scales, zeros, (int)N, G | R << 8, y, np.res_out, np.eps)
-  if (NT == 256) {
-    if (swiglu) LAQ_NORM_K(256, 1, true);
-    else if (RPL == 2) LAQ_NORM_K(256, 2, false);
-    else LAQ_NORM_K(256, 1, false);
+  if (NT == 256) {  // K <= 2048: one unit per thread
+    if (swiglu) LAQ_NORM_K(256, 1, true, 1);
+    else if (RPL == 2) LAQ_NORM_K(256, 2, false, 1);
+    else LAQ_NORM_K(256, 1, false, 1);
+  } else if (one_unit) {
+    if (swiglu) LAQ_NORM_K(512, 1, true, 1);
+    else if (RPL == 2) LAQ_NORM_K(512, 2, false, 1);
+    else LAQ_NORM_K(512, 1, false, 1);
   } else {
-    if (swiglu) LAQ_NORM_K(512, 1, true);
-    else if (RPL == 2) LAQ_NORM_K(512, 2, false);
-    else LAQ_NORM_K(512, 1, false);
+    if (swiglu) LAQ_NORM_K(512, 1, true, 2);
+    else if (RPL == 2) LAQ_NORM_K(512, 2, false, 2);
+    else LAQ_NORM_K(512, 1, false, 2);
   }
 #undef LAQ_NORM_K
   return hipGetLastError();
