@@ -166,7 +166,7 @@ def test_linear_swiglu(M, I, K, bits):
 NORM_LINEAR_CASES = [(3, False, 6144, 2560, True), (4, False, 6144, 2560, True), (3, False, 4100, 4096, True),
                      (3, False, 300, 8192, True), (3, False, 25000, 2560, True), (3, False, 1031, 2560, False),
                      (3, True, 2 * 9728, 2560, True), (4, True, 2 * 37, 1024, True), (3, True, 2 * 150, 8192, False),
-                     (3, False, 300, 128, True), (4, False, 517, 1024, False)]
+                     (3, False, 300, 128, True), (4, False, 517, 1024, False), (3, False, 40000, 2560, True)]
 
 
 @pytest.mark.parametrize("bits,swiglu,N,K,with_delta", NORM_LINEAR_CASES)
