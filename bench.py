@@ -361,7 +361,7 @@ def decode_step_extra(stack, dev, steps, context=1024):
         if i % 4 in (1, 3):
             q, sc, z = stack.q[3][i]
             f.residual_linear = lambda x, r_in, r_out, out: laq.linear_residual(x, q, sc, z, r_in, r_out, 3,
-                                                                                out=out)
+                                                                                write_out=False)
         return f
 
     mlp_ws = laq.mlp_workspace(D, I, dev)  # stream-ordered calls share it

@@ -376,7 +376,10 @@ laq_status laq_add_rmsnorm_linear_swiglu_w4g128(const float *residual, const voi
  * outputs the residual stream adds; Sec. 5, Table 3 setting).  The next
  * norm then reads the new residual with no delta (laq_add_rmsnorm_linear_*
  * with delta NULL).
- *   x, qweight, scales, zeros, y, N, K  as laq_linear_w3g128 with M = 1.
+ *   x, qweight, scales, zeros, N, K  as laq_linear_w3g128 with M = 1.
+ *   y             [out] fp16 [N], 2-byte aligned, or NULL: then only
+ *                 residual_out is written (a decode step whose next norm
+ *                 reads the residual alone needs no y).
  *   residual_in   [in] fp32 [N], 4-byte aligned.
  *   residual_out  [out] fp32 [N], 4-byte aligned; may be residual_in itself
  *                 (in place), otherwise must not overlap it.

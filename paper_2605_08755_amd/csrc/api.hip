@@ -403,7 +403,7 @@ laq_status linear_residual(const char* fn, const void* x, const uint32_t* qweigh
                            const uint8_t* zeros, void* y, const float* residual_in, float* residual_out, int64_t N,
                            int64_t K, void* stream) {
   const laq::LaunchEvents ev = take_events();
-  if (!x || !qweight || !scales || !zeros || !y || !residual_in || !residual_out)
+  if (!x || !qweight || !scales || !zeros || !residual_in || !residual_out)  // y may be NULL
     return fail(LAQ_ERR_NULL_POINTER, fn, "null pointer argument");
   laq_status st = check_shape(fn, N, K);
   if (st != LAQ_OK) return st;

@@ -610,7 +610,7 @@ __device__ __forceinline__ void flat_block(
         acc = row16_sum(acc);
         if (l == 0 && m < M) {
           const _Float16 yh = (_Float16)acc;
-          yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, yh);
+          if (!RES || yo != nullptr) yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, yh);
           if constexpr (RES) res_out[row0 + rr] = rres + (float)yh;
         }
       }
@@ -732,7 +732,7 @@ __device__ __forceinline__ void flat_block_rpl(
         acc = row16_sum(acc);
         if (l == 0 && m < M) {
           const _Float16 yh = (_Float16)acc;
-          yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, yh);
+          if (!RES || yo != nullptr) yo[(int64_t)m * N + row0 + rr] = __builtin_bit_cast(uint16_t, yh);
           if constexpr (RES) res_out[row0 + rr] = rres + (float)yh;
         }
       }
@@ -757,7 +757,8 @@ __global__ __launch_bounds__(NT) void linear_flat_kernel(
 }
 
 // Batch-1 linear with the residual output stage: y = x w_hat^T as
-// linear_flat_kernel computes it, and res_out[n] = res_in[n] + y[n].  The
+// linear_flat_kernel computes it, and res_out[n] = res_in[n] + y[n]; y may be
+// null, and then only res_out is written (one output stream less).  The
 // first fourteen dwords of arguments (preloaded) are what a wave needs before
 // its first requests, res_in included; fl(1/G) comes from v_rcp_f32, whose
 // error (one ulp) leaves trunc((t + 0.5) / G) exact for t < 1024 as in

@@ -60,8 +60,9 @@ class DecodeStep:
     (laq.add_rmsnorm_mlp, one kernel); the step then skips the down call.
     An o or down callable with an attribute residual_linear = g(x,
     residual_in, residual_out, out) adds its output to the residual stream
-    itself (laq.linear_residual: residual_out = residual_in + out); the next
-    norm then runs with no delta.
+    itself (laq.linear_residual: residual_out = residual_in + y); the next
+    norm then runs with no delta, so g need not write y to out (the step
+    reads only the residual; laq.linear_residual with write_out=False).
     """
 
     def __init__(self, shape, linears, norms, final_norm, k_caches, v_caches, device, lm_head=None,

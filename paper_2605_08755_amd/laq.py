@@ -235,10 +235,11 @@ def linear_noalloc_w3g128(x, qweight, scales, zeros, out=None):
     return y
 
 
-def linear_residual(x, qweight, scales, zeros, residual_in, residual_out, bits=3, out=None):
+def linear_residual(x, qweight, scales, zeros, residual_in, residual_out, bits=3, out=None, write_out=True):
     """One token's linear that also updates the residual stream: y = x @
     w_hat^T (fp16 [1][N], as `linear` computes it) and residual_out =
-    residual_in + y (fp32 [1][N]; may be residual_in itself)."""
+    residual_in + y (fp32 [1][N]; may be residual_in itself).  With
+    write_out=False only residual_out is written and None is returned."""
     import torch
     assert x.is_cuda and x.dtype == torch.float16 and x.dim() == 2 and x.shape[0] == 1 and x.is_contiguous()
     K = x.shape[1]
@@ -248,10 +249,12 @@ def linear_residual(x, qweight, scales, zeros, residual_in, residual_out, bits=3
     assert scales.dtype == torch.float16 and zeros.dtype == torch.uint8
     for r in (residual_in, residual_out):
         assert r.dtype == torch.float32 and r.numel() == N and r.is_contiguous()
-    y = torch.empty((1, N), dtype=torch.float16, device=x.device) if out is None else out
+    y = None
+    if write_out:
+        y = torch.empty((1, N), dtype=torch.float16, device=x.device) if out is None else out
     fn = lib().laq_linear_residual_w3g128 if bits == 3 else lib().laq_linear_residual_w4g128
-    _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), _ptr(residual_in), _ptr(residual_out), N,
-              K, _stream(x.device)))
+    _check(fn(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y) if y is not None else None,
+              _ptr(residual_in), _ptr(residual_out), N, K, _stream(x.device)))
     return y
 
 

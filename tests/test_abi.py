@@ -150,8 +150,10 @@ def _lres(L, bits, x=FAKE, q=FAKE, s=FAKE, z=FAKE, y=FAKE, ri=FAKE, ro=FAKE + 0x
 
 @pytest.mark.parametrize("bits", [3, 4])
 def test_linear_residual_validation(L, bits):
-    for kw in ("x", "q", "s", "z", "y", "ri", "ro"):
+    for kw in ("x", "q", "s", "z", "ri", "ro"):
         assert _lres(L, bits, **{kw: 0}) == laq.LAQ_ERR_NULL_POINTER
+    assert _lres(L, bits, y=0, N=0) == laq.LAQ_ERR_BAD_SHAPE          # y may be NULL (only the residual written)
+    assert _lres(L, bits, y=FAKE + 1) == laq.LAQ_ERR_MISALIGNED
     assert _lres(L, bits, N=0) == laq.LAQ_ERR_BAD_SHAPE
     assert _lres(L, bits, K=1920) == laq.LAQ_ERR_BAD_SHAPE          # fewer than 16 groups
     assert _lres(L, bits, K=32768) == laq.LAQ_ERR_BAD_SHAPE         # activation tile past the LDS budget

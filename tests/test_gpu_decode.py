@@ -215,7 +215,8 @@ def test_linear_residual(bits, N, K):
     """laq_linear_residual (a batch-1 linear that also writes residual_in + y
     to the residual stream): y against the oracle's linear within the linear
     tolerance and bit for bit equal to the plain laq_linear call; the new
-    residual bitwise equal to residual_in + y in fp32; in place as well.
+    residual bitwise equal to residual_in + y in fp32; in place as well, and
+    with y NULL (the residual alone written, bit for bit the same).
     Qwen3-4B's o (2560 x 4096) and down (2560 x 9728, two rows per lane), a
     ragged 4100 x 2048, 1000 x 8192, W4, 33 rows."""
     say("linear_residual", bits, N, K)
@@ -236,8 +237,11 @@ def test_linear_residual(bits, N, K):
     expect = res + y.cpu().numpy().astype(np.float32)
     assert np.array_equal(ro.cpu().numpy(), expect)
     assert np.array_equal(rd.cpu().numpy(), res)
+    ro2 = torch.full((1, N), float("nan"), dtype=torch.float32, device=DEV)
+    assert laq.linear_residual(dev(x), q, sd, zd, rd, ro2, bits, write_out=False) is None  # y NULL: residual only
     laq.linear_residual(dev(x), q, sd, zd, rd, rd, bits)  # in place
     torch.cuda.synchronize()
+    assert np.array_equal(ro2.cpu().numpy(), expect)
     assert np.array_equal(rd.cpu().numpy(), expect)
 
 
@@ -672,13 +676,15 @@ def test_decode_step_residual_producers_vs_oracle():
     each norm's residual is the last producer's (the token's embedding first)
     and its linear matches the oracle's linear on the oracle's RMSNorm of it;
     attention matches the oracle; three replays of a HIP-graph capture give
-    the eager logits bit for bit."""
+    the eager logits bit for bit, and so do producers that write only the
+    residual (y NULL)."""
     say("decode step with residual producers vs oracle")
     from paper_2605_08755_amd import decode
     shape = dict(decode.QWEN3_4B, layers=2, vocab=4096)
     D, Hq, Hkv, I, S, V, pos = shape["hidden"], shape["heads"], shape["kv_heads"], shape["mlp"], 256, 4096, 200
     rng = np.random.default_rng(31)
     rec = []
+    no_y = False
 
     def norm_lin(kind, l, q, s, z, swiglu):
         def f(x, out):  # unused by the step (norm_linear is present)
@@ -697,6 +703,9 @@ def test_decode_step_residual_producers_vs_oracle():
             laq.linear(x, q, s, z, 3, out=out)
 
         def g(x, r_in, r_out, out):
+            if no_y:  # the residual alone (y NULL), as a step that reads nothing else
+                laq.linear_residual(x, q, s, z, r_in, r_out, 3, write_out=False)
+                return
             laq.linear_residual(x, q, s, z, r_in, r_out, 3, out=out)
             rec.append({"kind": kind, "layer": l, "x": x.clone(), "res_in": r_in.clone(), "res_out": r_out.clone(),
                         "out": out.clone()})
@@ -780,3 +789,9 @@ def test_decode_step_residual_producers_vs_oracle():
         step.run(pos)
         torch.cuda.synchronize()
         assert torch.equal(step.logits.view(torch.int16), logits.view(torch.int16))
+    # the producers writing only the residual (y NULL): the same logits
+    no_y = True
+    step.logits.zero_()
+    step.run(pos)
+    torch.cuda.synchronize()
+    assert torch.equal(step.logits.view(torch.int16), logits.view(torch.int16))
