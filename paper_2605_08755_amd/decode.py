@@ -52,7 +52,8 @@ class DecodeStep:
     before it itself (laq.add_rmsnorm_linear: residual_out = residual + delta,
     out = RMSNorm(residual_out) * norm_weight, then the linear, one kernel);
     the step then skips that add_rmsnorm call and continues with the residual
-    in residual_out.  The step keeps two residual buffers for this;
+    in residual_out; when there is no delta the residual does not change and
+    the step passes residual_out None.  The step keeps two residual buffers for this;
     `residual` is the one holding the current residual stream.  A gate_up
     callable with an attribute norm_mlp (same arguments as norm_linear, out
     receiving the down projection's output, fp16 [1][hidden]) is the whole MLP
@@ -101,9 +102,13 @@ class DecodeStep:
         return self._res[self._cur]
 
     def _norm(self, f, delta, weight, out):
-        """Residual add + RMSNorm, then f: fused into f when it offers it."""
+        """Residual add + RMSNorm, then f: fused into f when it offers it.
+        With no delta the residual stays where it is (no residual_out)."""
         g = getattr(f, "norm_linear", None)
         if g is not None:
+            if delta is None:
+                g(self._res[self._cur], None, weight, self.s["eps"], None, out)
+                return
             g(self._res[self._cur], delta, weight, self.s["eps"], self._res[1 - self._cur], out)
             self._cur = 1 - self._cur
             return

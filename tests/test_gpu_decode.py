@@ -552,7 +552,7 @@ def test_decode_step_fused_norms_vs_oracle(merged_mlp):
         def g(res, delta, w, eps, res_out, out):
             laq.add_rmsnorm_linear(res, delta, w, eps, q, s, z, 3, swiglu=swiglu, out=out, residual_out=res_out)
             rec.append({"kind": kind, "layer": l, "res": res.clone(), "delta": None if delta is None else delta.clone(),
-                        "res_out": res_out.clone(), "out": out.clone()})
+                        "res_out": None if res_out is None else res_out.clone(), "out": out.clone()})
         f.norm_linear = g
         f.swiglu = swiglu
         return f
@@ -617,16 +617,22 @@ def test_decode_step_fused_norms_vs_oracle(merged_mlp):
         assert r["ok"], (name, r)
 
     def normed(e, w):
-        r_out = e["res"] + (e["delta"].astype(np.float32) if e["delta"] is not None else np.float32(0))
+        if e["delta"] is None:  # no delta: the residual stays put (no residual_out)
+            assert e["res_out"] is None
+            return np.asarray(OD.rmsnorm(e["res"], w, EPS)).astype(np.float16)
+        r_out = e["res"] + e["delta"].astype(np.float32)
         assert np.array_equal(e["res_out"], r_out)
         return np.asarray(OD.rmsnorm(r_out, w, EPS)).astype(np.float16)
+
+    def res_after(e):  # the residual stream after a norm
+        return e["res"] if e["res_out"] is None else e["res_out"]
 
     assert np.array_equal(g[("qkv", 0)]["res"], x0_h) and g[("qkv", 0)]["delta"] is None
     for l in range(2):
         w_in, w_post, qn, kn = norms_h[l]
         e_qkv, e_o, e_gu, e_dn = (g[(k, l)] for k in ("qkv", "o", "gu", "down"))
         if l > 0:
-            assert np.array_equal(e_qkv["res"], g[("gu", l - 1)]["res_out"])
+            assert np.array_equal(e_qkv["res"], res_after(g[("gu", l - 1)]))
             assert np.array_equal(e_qkv["delta"], g[("down", l - 1)]["out"])
         check(("qkv", l), e_qkv["out"], oracle.linear(normed(e_qkv, w_in), *host[l]["qkv"]))
         q_ref, k_ref, v_ref = OD.qk_norm_rope(e_qkv["out"], qn, kn, pos, Hq, Hkv, 128, EPS, THETA)
@@ -636,7 +642,7 @@ def test_decode_step_fused_norms_vs_oracle(merged_mlp):
         check(("attention", l), e_o["x"].reshape(Hq, 128),
               OD.decode_attention(q_ref.astype(np.float16), kc[:, :pos + 1], vc[:, :pos + 1]))
         check(("o", l), e_o["out"], oracle.linear(e_o["x"], *host[l]["o"]))
-        assert np.array_equal(e_gu["res"], e_qkv["res_out"]) and np.array_equal(e_gu["delta"], e_o["out"])
+        assert np.array_equal(e_gu["res"], res_after(e_qkv)) and np.array_equal(e_gu["delta"], e_o["out"])
         full = np.asarray(oracle.linear(normed(e_gu, w_post), *host[l]["gu"]), dtype=np.float64)
         h_ref = OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I)
         if merged_mlp:
@@ -646,9 +652,9 @@ def test_decode_step_fused_norms_vs_oracle(merged_mlp):
         assert np.array_equal(e_dn["x"], e_gu["out"])
         check(("down", l), e_dn["out"], oracle.linear(e_dn["x"], *host[l]["down"]))
     e_lm = g[("lm", 2)]
-    assert np.array_equal(e_lm["res"], g[("gu", 1)]["res_out"]) and np.array_equal(e_lm["delta"], g[("down", 1)]["out"])
+    assert np.array_equal(e_lm["res"], res_after(g[("gu", 1)])) and np.array_equal(e_lm["delta"], g[("down", 1)]["out"])
     check("logits", logits.cpu().numpy(), oracle.linear(normed(e_lm, fin_h), *h_lm))
-    assert np.array_equal(step.residual.cpu().numpy(), e_lm["res_out"])
+    assert np.array_equal(step.residual.cpu().numpy(), res_after(e_lm))
 
     # HIP graph of the same step (recording wrappers copy tensors, which the graph captures too)
     graph = torch.cuda.CUDAGraph()
@@ -693,7 +699,7 @@ def test_decode_step_residual_producers_vs_oracle():
         def g(res, delta, w, eps, res_out, out):
             laq.add_rmsnorm_linear(res, delta, w, eps, q, s, z, 3, swiglu=swiglu, out=out, residual_out=res_out)
             rec.append({"kind": kind, "layer": l, "res": res.clone(), "delta": None if delta is None else delta.clone(),
-                        "res_out": res_out.clone(), "out": out.clone()})
+                        "res_out": None if res_out is None else res_out.clone(), "out": out.clone()})
         f.norm_linear = g
         f.swiglu = swiglu
         return f
@@ -745,8 +751,7 @@ def test_decode_step_residual_producers_vs_oracle():
         assert r["ok"], (name, r)
 
     def normed(e, w):
-        assert e["delta"] is None
-        assert np.array_equal(e["res_out"], e["res"])
+        assert e["delta"] is None and e["res_out"] is None  # no delta: the residual stays put
         return np.asarray(OD.rmsnorm(e["res"], w, EPS)).astype(np.float16)
 
     def produced(e, hq):
@@ -765,12 +770,12 @@ def test_decode_step_residual_producers_vs_oracle():
         assert np.array_equal(vc[:, pos], v_ref.astype(np.float16))
         check(("attention", l), e_o["x"].reshape(Hq, 128),
               OD.decode_attention(q_ref.astype(np.float16), kc[:, :pos + 1], vc[:, :pos + 1]))
-        assert np.array_equal(e_o["res_in"], e_qkv["res_out"])
+        assert np.array_equal(e_o["res_in"], e_qkv["res"])
         produced(e_o, host[l]["o"])
         assert np.array_equal(e_gu["res"], e_o["res_out"])
         full = np.asarray(oracle.linear(normed(e_gu, w_post), *host[l]["gu"]), dtype=np.float64)
         check(("gate|up + silu", l), e_gu["out"], OD.silu_mul(np.concatenate([full[:, 0::2], full[:, 1::2]], axis=1), I))
-        assert np.array_equal(e_dn["x"], e_gu["out"]) and np.array_equal(e_dn["res_in"], e_gu["res_out"])
+        assert np.array_equal(e_dn["x"], e_gu["out"]) and np.array_equal(e_dn["res_in"], e_gu["res"])
         produced(e_dn, host[l]["down"])
         res_prev = e_dn["res_out"]
     e_lm = g[("lm", 2)]
