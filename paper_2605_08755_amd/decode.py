@@ -53,8 +53,10 @@ class DecodeStep:
     out = RMSNorm(residual_out) * norm_weight, then the linear, one kernel);
     the step then skips that add_rmsnorm call and continues with the residual
     in residual_out; when there is no delta the residual does not change and
-    the step passes residual_out None.  The step keeps two residual buffers for this;
-    `residual` is the one holding the current residual stream.  A gate_up
+    the step passes residual_out None.  The step keeps two residual buffers for this
+    besides x0, which it reads in place and never writes (the first update
+    goes to a buffer); `residual` is the tensor holding the current residual
+    stream.  A gate_up
     callable with an attribute norm_mlp (same arguments as norm_linear, out
     receiving the down projection's output, fp16 [1][hidden]) is the whole MLP
     block after the attention: norm, gate|up, SiLU-and-multiply and down
@@ -78,8 +80,8 @@ class DecodeStep:
         self.cos_sin = rope_table(S_max, shape["rope_theta"], device)
         f16 = dict(dtype=torch.float16, device=device)
         self._res = [torch.zeros((1, D), dtype=torch.float32, device=device) for _ in range(2)]
-        self._cur = 0
         self.x0 = torch.zeros((1, D), dtype=torch.float32, device=device)  # the token's embedding
+        self._r = self.x0  # the tensor holding the residual stream (x0 until the first update)
         self.h = torch.empty((1, D), **f16)
         self.qkv = torch.empty((1, (Hq + 2 * Hkv) * HEAD_DIM), **f16)
         self.q = torch.empty((Hq, HEAD_DIM), **f16)
@@ -99,7 +101,20 @@ class DecodeStep:
     @property
     def residual(self):
         """fp32 [1][hidden]: the residual stream as of the last call issued."""
-        return self._res[self._cur]
+        return self._r
+
+    def _next(self):
+        """The residual buffer the next update writes: never x0 (read-only
+        input of every step) and never the current residual."""
+        return self._res[1] if self._r is self._res[0] else self._res[0]
+
+    def _in_place(self):
+        """The current residual, made writable for an in-place update."""
+        if self._r is self.x0:
+            nxt = self._next()
+            nxt.copy_(self.x0)
+            self._r = nxt
+        return self._r
 
     def _norm(self, f, delta, weight, out):
         """Residual add + RMSNorm, then f: fused into f when it offers it.
@@ -107,12 +122,13 @@ class DecodeStep:
         g = getattr(f, "norm_linear", None)
         if g is not None:
             if delta is None:
-                g(self._res[self._cur], None, weight, self.s["eps"], None, out)
+                g(self._r, None, weight, self.s["eps"], None, out)
                 return
-            g(self._res[self._cur], delta, weight, self.s["eps"], self._res[1 - self._cur], out)
-            self._cur = 1 - self._cur
+            nxt = self._next()
+            g(self._r, delta, weight, self.s["eps"], nxt, out)
+            self._r = nxt
             return
-        laq.add_rmsnorm(self._res[self._cur], delta, weight, self.s["eps"], out=self.h)
+        laq.add_rmsnorm(self._in_place(), delta, weight, self.s["eps"], out=self.h)  # (writes the residual)
         f(self.h, out)
 
     def _linear(self, f, x, out):
@@ -122,8 +138,9 @@ class DecodeStep:
         if g is None:
             f(x, out)
             return out
-        g(x, self._res[self._cur], self._res[1 - self._cur], out)
-        self._cur = 1 - self._cur
+        nxt = self._next()
+        g(x, self._r, nxt, out)
+        self._r = nxt
         return None
 
     def run(self, pos):
@@ -132,8 +149,7 @@ class DecodeStep:
         norm's output."""
         s = self.s
         Hq, Hkv, eps = s["heads"], s["kv_heads"], s["eps"]
-        self._cur = 0
-        self._res[0].copy_(self.x0)
+        self._r = self.x0  # read in place: the first update writes another buffer
         delta = None
         for l, (f_qkv, f_o, f_gu, f_down) in enumerate(self.linears):
             w_in, w_post, qn, kn = self.norms[l]
@@ -149,8 +165,9 @@ class DecodeStep:
             delta = self._linear(f_o, self.attn.view(1, Hq * HEAD_DIM), self.o)
             mlp = getattr(f_gu, "norm_mlp", None)
             if mlp is not None:
-                mlp(self._res[self._cur], delta, w_post, eps, self._res[1 - self._cur], self.down)
-                self._cur = 1 - self._cur
+                nxt = self._next()
+                mlp(self._r, delta, w_post, eps, nxt, self.down)
+                self._r = nxt
                 delta = self.down
                 continue
             if getattr(f_gu, "swiglu", False):
@@ -162,7 +179,7 @@ class DecodeStep:
         if self.lm_head is not None and getattr(self.lm_head, "norm_linear", None) is not None:
             self._norm(self.lm_head, delta, self.final_norm, self.logits)
             return self.logits
-        laq.add_rmsnorm(self._res[self._cur], delta, self.final_norm, eps, out=self.out)
+        laq.add_rmsnorm(self._in_place(), delta, self.final_norm, eps, out=self.out)
         if self.lm_head is None:
             return self.out
         self.lm_head(self.out, self.logits)
